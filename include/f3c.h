@@ -1,0 +1,242 @@
+/*
+ * f3c — geometry-aware cached sampling of a sparse-structure flow transformer
+ * (Fast3Dcache, arXiv 2511.22533) on AMD Instinct MI355X (gfx950).
+ *
+ * C ABI. Plain pointers and sizes only. "dev" pointers are device (HBM)
+ * addresses, "host" pointers are CPU memory. Streams are HIP streams passed as
+ * opaque pointers (NULL = the default stream). Every call that enqueues device
+ * work is asynchronous with respect to the host, ordered on the given stream,
+ * and never synchronises the device or copies device memory back to the host
+ * unless its comment says so.
+ *
+ * Errors: every int-returning call returns F3C_OK (0) or a negative code, and
+ * sets a thread-local message readable with f3c_last_error(). All arguments are
+ * validated before any device work is enqueued, so a failed call has no device
+ * side effects. F3C_EHIP reports a HIP runtime failure (launch or copy).
+ *
+ * Memory ownership: the library never allocates device memory. The caller
+ * allocates the weight buffer and the state buffer (sizes from
+ * f3c_model_weights_bytes / f3c_state_bytes, 256-byte aligned) and keeps them
+ * alive until the model / state is destroyed. Host-side objects (f3c_model,
+ * f3c_state) are owned by the library and released by the destroy calls.
+ *
+ * Layouts: latent grids and velocities are float32 [B][N][8], token-major,
+ * with token n = (z*G + y)*G + x for an G x G x G grid (the flatten order of
+ * the D x H x W latent, Sec. 4.2). Condition tokens are float32 [B][Nc][dc].
+ */
+#ifndef F3C_H
+#define F3C_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define F3C_OK 0
+#define F3C_EINVAL (-1)   /* bad argument, shape or value */
+#define F3C_ENOMEM (-2)   /* caller-provided buffer too small */
+#define F3C_EHIP (-3)     /* HIP runtime error */
+#define F3C_ESTATE (-4)   /* call out of order (weights not loaded, condition not set) */
+
+#define F3C_F32 0         /* float32 compute (debug / small models) */
+#define F3C_BF16 1        /* bfloat16 operands, float32 accumulation and residual */
+
+#define F3C_MAX_BATCH 64
+#define F3C_MAX_TOKENS 32768
+
+typedef void* f3c_stream; /* hipStream_t */
+
+/* Model shape. Sec. 3.2: the sparse-structure flow transformer evolves a latent
+ * grid S in R^{B x C x D x H x W} under image conditioning; the per-block
+ * contents follow the supplement's FLOPs list (6*D modulation, three
+ * LayerNorms, self-attention, cross-attention to D_cond-wide condition tokens,
+ * ratio-4 MLP). Constraints: in_ch == 8, grid^3 <= F3C_MAX_TOKENS,
+ * width = heads * head_dim with head_dim in {32, 64}, width a multiple of 128
+ * and at most 2048, cond_width a multiple of 64, mlp_ratio in 1..8. */
+typedef struct {
+  int32_t grid;
+  int32_t in_ch;
+  int32_t width;
+  int32_t depth;
+  int32_t heads;
+  int32_t mlp_ratio;
+  int32_t cond_tokens;
+  int32_t cond_width;
+  int32_t dtype;          /* F3C_F32 or F3C_BF16 */
+} f3c_model_cfg;
+
+typedef struct f3c_model f3c_model;
+typedef struct f3c_state f3c_state;
+
+/* Thread-local message describing the last failed call on this thread. */
+const char* f3c_last_error(void);
+int f3c_version(void);
+
+/* ------------------------------------------------------------------ model */
+
+/* Validate cfg and create a host-side model object. No device work. */
+int f3c_model_create(const f3c_model_cfg* cfg, f3c_model** out);
+void f3c_model_destroy(f3c_model* m);
+
+/* Canonical parameter list, in load order: name (static string) and element
+ * count. Linear weights are [out][in]; names ending in "_b" are biases. */
+int f3c_weight_count(const f3c_model* m, int32_t* n);
+int f3c_weight_info(const f3c_model* m, int32_t i, const char** name, int64_t* numel);
+
+/* Device bytes needed for the weights of this model. */
+int f3c_model_weights_bytes(const f3c_model* m, size_t* bytes);
+
+/* Bind a caller-allocated device buffer (>= f3c_model_weights_bytes) and upload
+ * the parameters from host float32 arrays given in canonical order. Matrices are
+ * rounded to the model dtype (round-to-nearest-even for bf16); biases stay f32.
+ * Synchronous: returns after the upload completed. */
+int f3c_model_load_weights(f3c_model* m, void* weights_dev, size_t bytes, const float* const* host_f32,
+                           int32_t n);
+
+/* FLOPs model of the supplement (FLOPs Calculation) for one forward over n_tok
+ * tokens per sample, summed over blocks (modulation, 3 LN, SA, CA, MLP). */
+double f3c_forward_flops(const f3c_model_cfg* cfg, int32_t n_tok, int32_t batch);
+
+/* ------------------------------------------------------------------ state */
+
+/* Device bytes for a sampler state of `batch` samples: the velocity cache pair,
+ * activations of a full step, the per-sample condition keys/values and the
+ * selection buffers. */
+int f3c_state_bytes(const f3c_model* m, int32_t batch, size_t* bytes);
+
+/* Create a state over a caller-allocated device buffer. The caches are zeroed
+ * on `stream` (Algorithm 1 initialises v_cache to 0). omega defaults to 0.7. */
+int f3c_state_create(f3c_model* m, int32_t batch, void* state_dev, size_t bytes, f3c_stream stream,
+                     f3c_state** out);
+void f3c_state_destroy(f3c_state* s);
+
+/* Zero both velocity caches (start of a new trajectory). */
+int f3c_state_reset(f3c_state* s, f3c_stream stream);
+
+/* SSC weight omega of Eq. (6), in [0, 1]. */
+int f3c_state_set_omega(f3c_state* s, float omega);
+
+/* Precompute the cross-attention keys/values of every block from the condition
+ * tokens cond_dev (float32 [B][Nc][dc], device). They depend only on the
+ * condition and the weights, so one call serves the whole trajectory. */
+int f3c_set_cond(f3c_state* s, const float* cond_dev, f3c_stream stream);
+
+/* One denoising step of Algorithm 1 with every token active (Phase 1, Phase 3
+ * correction steps): v = G(x_t, t, c); x <- x - (t - t_next) v; caches rotate.
+ * x_dev: float32 [B][N][8], updated in place. Requires t > t_next, both finite. */
+int f3c_full_step(f3c_state* s, float* x_dev, double t, double t_next, f3c_stream stream);
+
+/* One cached denoising step of Algorithm 1. n_cache_host[b] in [0, N] is the
+ * number of tokens of sample b whose velocity is reused (the quota c_t of
+ * Eq. 5 / Phase 3, a count of cached tokens). The c_b tokens with the lowest
+ * stability score (Eq. 6; ties -> smaller token index) are cached; the
+ * transformer runs on the remaining tokens only, self-attention within each
+ * sample's active set; cached rows keep their stored velocity bit for bit.
+ * With every n_cache_host[b] == 0 it computes exactly what f3c_full_step does. */
+int f3c_cached_step(f3c_state* s, float* x_dev, double t, double t_next, const int32_t* n_cache_host,
+                    f3c_stream stream);
+
+/* Device views of the state (valid until the next step call):
+ * v_cache / v_prev float32 [B][N][8]; idx_active int32 [sum n_b]; pos int32
+ * [B][N] (packed active row or -1); v_act float32 [sum n_b][8]; mod float32
+ * [L][6][width]; score float32 [B][N] (written only while score recording is
+ * on). act_off_host receives the B+1 active-row offsets of the last step. */
+int f3c_state_views(const f3c_state* s, float** v_cache, float** v_prev, int32_t** idx_active, int32_t** pos,
+                    float** v_act, float** mod, float** score, int32_t* act_off_host);
+int f3c_state_record_scores(f3c_state* s, int32_t on);
+
+/* Checkpoint: the sampler state beyond x is the cache pair. export copies
+ * v_cache then v_prev (2*B*N*8 floats) to host memory; import restores them.
+ * Both synchronise `stream`. */
+int f3c_state_export(const f3c_state* s, float* host, size_t n_floats, f3c_stream stream);
+int f3c_state_import(f3c_state* s, const float* host, size_t n_floats, f3c_stream stream);
+
+/* Per-kernel-class timing with HIP events recorded around each launch on the
+ * launch stream while enabled. read synchronises the recorded events and
+ * returns launches, total milliseconds and total algorithmic FLOPs (dense
+ * contractions: 2*M*N*K; attention: the QK^T and PV terms of the FLOPs model)
+ * and algorithmic bytes (memory-bound kernels). */
+#define F3C_PROF_SELECT 0
+#define F3C_PROF_EMBED 1
+#define F3C_PROF_MOD 2
+#define F3C_PROF_LN 3
+#define F3C_PROF_GEMM_QKV 4
+#define F3C_PROF_ATTN_SELF 5
+#define F3C_PROF_GEMM_O 6
+#define F3C_PROF_GEMM_Q 7
+#define F3C_PROF_ATTN_CROSS 8
+#define F3C_PROF_GEMM_CO 9
+#define F3C_PROF_GEMM_FC1 10
+#define F3C_PROF_GEMM_FC2 11
+#define F3C_PROF_FINAL 12
+#define F3C_PROF_EULER 13
+#define F3C_PROF_COND 14
+#define F3C_PROF_CLASSES 15
+int f3c_profile_enable(f3c_state* s, int32_t on);
+int f3c_profile_read(f3c_state* s, int32_t cls, int64_t* launches, double* ms, double* flops, double* bytes);
+int f3c_profile_reset(f3c_state* s);
+
+/* ------------------------------------------------------- operator entry points
+ * The individual kernels of the step on caller buffers, for parity testing of
+ * each stage. Same conventions; dtype is F3C_F32 or F3C_BF16 and names the
+ * element type of the "T" buffers. */
+
+/* SSC scoring + selection (Eqs. 2, 6, 7; Algorithm 1 SSC) for B samples of N
+ * tokens: v_cache, v_prev float32 [B][N][8]; n_cache_host[b] in [0, N]. Writes
+ * idx_active (int32, sum(N - c_b) rows, ascending per sample), pos int32 [B][N]
+ * and, if score != NULL, score float32 [B][N] (for samples with c_b > 0). */
+int f3c_op_select(int32_t batch, int32_t n_tokens, const float* v_cache, const float* v_prev, float omega,
+                  const int32_t* n_cache_host, int32_t* idx_active, int32_t* pos, float* score, f3c_stream stream);
+
+/* out/resid = A W^T + bias (+ epilogue). A: T [M][lda], W: T [N][ldw], bias f32 [N].
+ * epilogue 0: out T [M][ldo] = value; 1: out = GELU_tanh(value);
+ * 2: resid f32 [M][ldr] += (gate ? gate[n] : 1) * value.
+ * Requires N % 128 == 0, K a multiple of 64 (bf16) / 32 (f32), 16-byte aligned rows. */
+int f3c_op_gemm(int32_t dtype, int32_t epilogue, int32_t M, int32_t N, int32_t K, const void* A, int32_t lda,
+                const void* W, int32_t ldw, const float* bias, const float* gate, void* out, int32_t ldo,
+                float* resid, int32_t ldr, f3c_stream stream);
+
+/* Varlen multi-head attention: sample b's queries are rows q_off[b]..q_off[b+1]
+ * of q (T, row stride ldq), its keys/values rows k_off[b]..k_off[b+1] of k/v;
+ * head h uses columns h*head_dim..; o (T) gets one row per query.
+ * head_dim in {32, 64}; offsets are host arrays of B+1 non-decreasing ints. */
+int f3c_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int32_t batch, const int32_t* q_off_host,
+                     const int32_t* k_off_host, const void* q, int32_t ldq, const void* k, int32_t ldk,
+                     const void* v, int32_t ldv, void* o, int32_t ldo, f3c_stream stream);
+
+/* out T [rows][d] = LN(h) * (1 + scale) + shift (no affine LN, eps 1e-6);
+ * shift/scale f32 [d] or both NULL. d in {128, 256, 512, 1024, 2048}. */
+int f3c_op_ln_mod(int32_t dtype, int32_t rows, int32_t d, const float* h, const float* shift, const float* scale,
+                  void* out, f3c_stream stream);
+
+/* Time embedding + all block modulations for time t into mod (f32 [L][6][width]). */
+int f3c_op_modulation(const f3c_model* m, double t, float* mod_dev, float* scratch_dev /* 2*width f32 */,
+                      f3c_stream stream);
+
+/* ----------------------------------------------------------- host schedules */
+
+/* Timestep grid t_k = shift(1 - (k-1)/T), k = 1..T+1 (Eq. S1 with factor eta;
+ * eta = 1 is uniform). out_host receives T+1 doubles. */
+int f3c_time_grid(int32_t steps, double eta, double* out_host);
+
+/* ceil(steps * rho) for a decimal ratio rho (anchor step with rho_a, guidance-off
+ * step with rho_CFG-OFF). */
+int32_t f3c_ceil_ratio(int32_t steps, double rho);
+
+/* Eqs. (4)-(5): floor(N - sigma * exp(mu * (k - k_anchor)) / gamma_up) clamped to [0, N]. */
+int32_t f3c_pcsc_quota(int32_t k, int32_t n_tokens, double sigma, double mu, int32_t k_anchor, double gamma_up);
+
+/* Algorithm 1, step 1: cached count for step k (1-based): 0 in Phase 1
+ * (k <= ceil(T rho_a)); n_cache_phase2 in Phase 2 (k < ceil(T rho_off));
+ * in Phase 3, 0 when (k - ceil(T rho_off) + 1) mod f_corr == 0 (f_corr > 0),
+ * else floor(N * xi). */
+int32_t f3c_phase_quota(int32_t k, int32_t steps, int32_t n_tokens, int32_t n_cache_phase2, double rho_a,
+                        double rho_off, double xi, int32_t f_corr);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* F3C_H */

@@ -1,0 +1,68 @@
+// Shared device-side definitions for the gfx950 kernels: element types, MFMA
+// fragment traits for the 32x32 matrix-core family, and small helpers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace f3c {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// 32x32 MFMA family. One instruction multiplies a 32xK by a Kx32 tile. Each
+// lane l feeds E consecutive K-elements of row (A) / column (B) l % 32 for the
+// K-group l / 32; the 16 accumulators of lane l hold column l % 32 and rows
+// 8*(i/4) + 4*(l/32) + i%4, i = 0..15.
+template <typename T> struct Mfma;
+
+template <> struct Mfma<bf16> {
+  static constexpr int E = 8;          // elements per lane per instruction (K = 16)
+  typedef bf16x8 frag;
+  static __device__ __forceinline__ f32x16 mma(const frag& a, const frag& b, const f32x16& c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+};
+
+template <> struct Mfma<float> {
+  static constexpr int E = 1;          // K = 2
+  typedef float frag;
+  static __device__ __forceinline__ f32x16 mma(const frag& a, const frag& b, const f32x16& c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+};
+
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16 x) { return static_cast<float>(x); }
+
+template <typename T> __device__ __forceinline__ T from_f32(float x);
+template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return static_cast<bf16>(x); }
+
+__device__ __forceinline__ float gelu_tanh(float x) {
+  const float k0 = 0.7978845608028654f;   // sqrt(2/pi)
+  const float k1 = 0.044715f;
+  return 0.5f * x * (1.0f + tanhf(k0 * (x + k1 * x * x * x)));
+}
+
+__device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// Sample lookup in a segment table off[0..B] (off[B] = total rows).
+__device__ __forceinline__ int find_segment(const int* off, int B, int row) {
+  int b = 0;
+  while (b + 1 < B && off[b + 1] <= row) ++b;
+  return b;
+}
+
+}  // namespace f3c

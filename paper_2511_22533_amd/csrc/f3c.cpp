@@ -1,0 +1,760 @@
+// Host side of the f3c C ABI: argument validation, weight and state layout in
+// caller-provided device memory, and the stream-ordered orchestration of one
+// cached denoising step (Algorithm 1): select -> gather/embed -> modulation ->
+// L blocks on the compacted set -> final projection -> merge/Euler/rotate.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/f3c.h"
+#include "kernels.h"
+
+using namespace f3c;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define HIP_TRY(expr)                                                                  \
+  do {                                                                                 \
+    hipError_t e_ = (expr);                                                            \
+    if (e_ != hipSuccess) return fail(F3C_EHIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct Spec {
+  std::string name;
+  int64_t rows, cols;   // cols == 0 for vectors
+  bool bias;
+  size_t off = 0;       // byte offset in the weight buffer
+  int64_t numel() const { return cols ? rows * cols : rows; }
+};
+
+}  // namespace
+
+struct f3c_model {
+  f3c_model_cfg cfg;
+  int N, d, hd, dm, L, dc, Nc;
+  size_t es;
+  std::vector<Spec> specs;
+  size_t wbytes = 0;
+  char* wdev = nullptr;
+  bool loaded = false;
+  // group bases (bytes)
+  size_t mod_w, mod_b, kv_w, kv_b;
+
+  const void* w(const std::string& name) const {
+    for (const auto& s : specs)
+      if (s.name == name) return wdev + s.off;
+    return nullptr;
+  }
+  const float* b(const std::string& name) const { return static_cast<const float*>(w(name)); }
+};
+
+struct Prof {
+  std::vector<hipEvent_t> ev;       // start/stop pairs
+  int64_t launches = 0;
+  double flops = 0, bytes = 0;
+};
+
+struct f3c_state {
+  f3c_model* m;
+  int B;
+  char* dev;
+  size_t bytes;
+  float* v[2];
+  int cur = 0;
+  float *h, *vact, *mod, *temb, *score;
+  void *u, *qkv, *att, *qc, *hid, *cond_t, *kv;
+  int32_t *idx, *pos;
+  bool cond_set = false, record_scores = false, profiling = false;
+  float omega = 0.7f;
+  Segs last_act{};
+  Prof prof[F3C_PROF_CLASSES];
+  std::vector<hipEvent_t> pool;
+};
+
+namespace {
+
+hipEvent_t take_event(f3c_state* s) {
+  if (!s->pool.empty()) {
+    hipEvent_t e = s->pool.back();
+    s->pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Records an event pair around one launch when profiling is on.
+struct Scope {
+  f3c_state* s;
+  int cls;
+  hipStream_t st;
+  hipEvent_t e1 = nullptr;
+  Scope(f3c_state* s_, int cls_, hipStream_t st_, double flops, double bytes) : s(s_), cls(cls_), st(st_) {
+    if (!s->profiling) return;
+    hipEvent_t e0 = take_event(s);
+    e1 = take_event(s);
+    if (!e0 || !e1) { e1 = nullptr; return; }
+    (void)hipEventRecord(e0, st);
+    s->prof[cls].ev.push_back(e0);
+    s->prof[cls].launches += 1;
+    s->prof[cls].flops += flops;
+    s->prof[cls].bytes += bytes;
+  }
+  ~Scope() {
+    if (!e1) return;
+    (void)hipEventRecord(e1, st);
+    s->prof[cls].ev.push_back(e1);
+  }
+};
+
+int validate_cfg(const f3c_model_cfg* c) {
+  if (!c) return fail(F3C_EINVAL, "cfg is NULL");
+  if (c->dtype != F3C_F32 && c->dtype != F3C_BF16) return fail(F3C_EINVAL, "dtype must be F3C_F32 or F3C_BF16");
+  if (c->in_ch != 8) return fail(F3C_EINVAL, "in_ch must be 8 (got %d)", c->in_ch);
+  if (c->grid < 1) return fail(F3C_EINVAL, "grid must be >= 1");
+  const int64_t n = (int64_t)c->grid * c->grid * c->grid;
+  if (n > F3C_MAX_TOKENS) return fail(F3C_EINVAL, "grid^3 = %lld exceeds %d tokens", (long long)n, F3C_MAX_TOKENS);
+  if (c->heads < 1 || c->width % c->heads) return fail(F3C_EINVAL, "width must be a multiple of heads");
+  const int hd = c->width / c->heads;
+  if (hd != 32 && hd != 64) return fail(F3C_EINVAL, "head_dim must be 32 or 64 (got %d)", hd);
+  if (c->width % 128 || c->width > 2048) return fail(F3C_EINVAL, "width must be a multiple of 128, <= 2048");
+  if ((c->width / 64) & ((c->width / 64) - 1)) return fail(F3C_EINVAL, "width/64 must be a power of two");
+  if (c->depth < 1 || c->depth > 256) return fail(F3C_EINVAL, "depth must be in 1..256");
+  if (c->mlp_ratio < 1 || c->mlp_ratio > 8) return fail(F3C_EINVAL, "mlp_ratio must be in 1..8");
+  if (c->cond_tokens < 1 || c->cond_tokens > 65536) return fail(F3C_EINVAL, "cond_tokens must be in 1..65536");
+  if (c->cond_width < 64 || c->cond_width % 64) return fail(F3C_EINVAL, "cond_width must be a multiple of 64");
+  return F3C_OK;
+}
+
+uint16_t f32_to_bf16_bits(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;   // NaN
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+double block_flops(int B, double n, double d, double H, double nc, double dc, double dm) {
+  const double mod = 5 * B * d + 2 * B * d * 6 * d;
+  const double ln = 3 * 7 * B * n * d;
+  const double sa = 2 * B * n * d * 3 * d + 2 * B * H * n * n * (d / H) + 5 * B * H * n * n +
+                    2 * B * H * n * n * (d / H) + 2 * B * n * d * d;
+  const double ca = 2 * B * n * d * d + 2 * B * nc * dc * 2 * d + 2 * B * H * n * nc * (d / H) + 5 * B * H * n * nc +
+                    2 * B * H * n * nc * (d / H) + 2 * B * n * d * d;
+  const double mlp = 2 * B * n * d * dm + 5 * B * n * dm + 2 * B * n * dm * d;
+  return mod + ln + sa + ca + mlp;
+}
+
+int check_state(f3c_state* s) {
+  if (!s) return fail(F3C_EINVAL, "state is NULL");
+  if (!s->m->loaded) return fail(F3C_ESTATE, "weights not loaded");
+  return F3C_OK;
+}
+
+int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_cache, hipStream_t st) {
+  f3c_model* m = s->m;
+  const int B = s->B, N = m->N, d = m->d, L = m->L, dt = m->cfg.dtype;
+  const size_t es = m->es;
+  Segs act{}, quota{}, cond_segs{};
+  act.B = quota.B = cond_segs.B = B;
+  bool any_cached = false;
+  for (int b = 0; b < B; ++b) {
+    const int c = n_cache ? n_cache[b] : 0;
+    quota.off[b] = c;
+    act.off[b + 1] = act.off[b] + (N - c);
+    cond_segs.off[b + 1] = cond_segs.off[b] + m->Nc;
+    any_cached |= c > 0;
+  }
+  const int rows = act.off[B];
+  float* v_cache = s->v[s->cur];
+  float* v_prev = s->v[1 - s->cur];
+  const int32_t* idx = nullptr;
+  const int32_t* pos = nullptr;
+
+  if (any_cached) {
+    const float w_a = s->omega, w_v = 1.0f - w_a;
+    Scope sc(s, F3C_PROF_SELECT, st, 0, (double)B * N * (64 + 4) + rows * 4.0);
+    HIP_TRY(launch_select(v_cache, v_prev, B, N, w_a, w_v, quota, act, s->idx, s->pos,
+                          s->record_scores ? s->score : nullptr, st));
+    idx = s->idx;
+    pos = s->pos;
+  }
+  {
+    Scope sc(s, F3C_PROF_MOD, st, 0, (double)es * d * (256 + d + 6.0 * L * d));
+    const char* mw = m->wdev;
+    HIP_TRY(launch_gemv(dt, m->w("t1_w"), m->b("t1_b"), nullptr, t, GEMV_IN_TIMESTEP, 1, d, 256, s->temb, st));
+    HIP_TRY(launch_gemv(dt, m->w("t2_w"), m->b("t2_b"), s->temb, 0.0, GEMV_IN_PLAIN, 1, d, d, s->temb + d, st));
+    HIP_TRY(launch_gemv(dt, mw + m->mod_w, (const float*)(mw + m->mod_b), s->temb + d, 0.0, GEMV_IN_PLAIN, 0,
+                        6 * L * d, d, s->mod, st));
+  }
+  if (rows > 0) {
+    {
+      Scope sc(s, F3C_PROF_EMBED, st, 0, rows * (32.0 + d * es + d * 4.0));
+      HIP_TRY(launch_embed(dt, x, N, idx, act, m->w("in_w"), m->b("in_b"), m->w("pos"), d, s->h, st));
+    }
+    const int dm = m->dm;
+    const double lnb = rows * (double)d * (4 + es);
+    for (int l = 0; l < L; ++l) {
+      const std::string p = "blk" + std::to_string(l) + ".";
+      const float* md = s->mod + (size_t)l * 6 * d;
+      {
+        Scope sc(s, F3C_PROF_LN, st, 0, lnb);
+        HIP_TRY(launch_ln_mod(dt, s->h, rows, d, md, md + d, s->u, st));
+      }
+      {
+        Scope sc(s, F3C_PROF_GEMM_QKV, st, 2.0 * rows * 3 * d * d, 0);
+        HIP_TRY(launch_gemm(dt, EPI_STORE, rows, 3 * d, d, s->u, d, m->w(p + "qkv_w"), d, m->b(p + "qkv_b"),
+                            nullptr, s->qkv, 3 * d, nullptr, 0, st));
+      }
+      {
+        double fl = 0;
+        for (int b = 0; b < B; ++b) fl += 4.0 * (double)(act.off[b + 1] - act.off[b]) * (act.off[b + 1] - act.off[b]) * d;
+        Scope sc(s, F3C_PROF_ATTN_SELF, st, fl, 0);
+        const char* q = static_cast<const char*>(s->qkv);
+        HIP_TRY(launch_attention(dt, m->cfg.heads, m->hd, act, act, q, 3 * d, q + d * es, 3 * d, q + 2 * d * es,
+                                 3 * d, s->att, d, st));
+      }
+      {
+        Scope sc(s, F3C_PROF_GEMM_O, st, 2.0 * rows * d * d, 0);
+        HIP_TRY(launch_gemm(dt, EPI_RESID, rows, d, d, s->att, d, m->w(p + "o_w"), d, m->b(p + "o_b"), md + 2 * d,
+                            nullptr, 0, s->h, d, st));
+      }
+      {
+        Scope sc(s, F3C_PROF_LN, st, 0, lnb);
+        HIP_TRY(launch_ln_mod(dt, s->h, rows, d, nullptr, nullptr, s->u, st));
+      }
+      {
+        Scope sc(s, F3C_PROF_GEMM_Q, st, 2.0 * rows * d * d, 0);
+        HIP_TRY(launch_gemm(dt, EPI_STORE, rows, d, d, s->u, d, m->w(p + "q_w"), d, m->b(p + "q_b"), nullptr,
+                            s->qc, d, nullptr, 0, st));
+      }
+      {
+        Scope sc(s, F3C_PROF_ATTN_CROSS, st, 4.0 * rows * m->Nc * d, 0);
+        const char* kv = static_cast<const char*>(s->kv) + (size_t)l * 2 * d * es;
+        HIP_TRY(launch_attention(dt, m->cfg.heads, m->hd, act, cond_segs, s->qc, d, kv, 2 * L * d, kv + d * es,
+                                 2 * L * d, s->att, d, st));
+      }
+      {
+        Scope sc(s, F3C_PROF_GEMM_CO, st, 2.0 * rows * d * d, 0);
+        HIP_TRY(launch_gemm(dt, EPI_RESID, rows, d, d, s->att, d, m->w(p + "co_w"), d, m->b(p + "co_b"), nullptr,
+                            nullptr, 0, s->h, d, st));
+      }
+      {
+        Scope sc(s, F3C_PROF_LN, st, 0, lnb);
+        HIP_TRY(launch_ln_mod(dt, s->h, rows, d, md + 3 * d, md + 4 * d, s->u, st));
+      }
+      {
+        Scope sc(s, F3C_PROF_GEMM_FC1, st, 2.0 * rows * dm * d, 0);
+        HIP_TRY(launch_gemm(dt, EPI_GELU, rows, dm, d, s->u, d, m->w(p + "fc1_w"), d, m->b(p + "fc1_b"), nullptr,
+                            s->hid, dm, nullptr, 0, st));
+      }
+      {
+        Scope sc(s, F3C_PROF_GEMM_FC2, st, 2.0 * rows * d * dm, 0);
+        HIP_TRY(launch_gemm(dt, EPI_RESID, rows, d, dm, s->hid, dm, m->w(p + "fc2_w"), dm, m->b(p + "fc2_b"),
+                            md + 5 * d, nullptr, 0, s->h, d, st));
+      }
+    }
+    {
+      Scope sc(s, F3C_PROF_FINAL, st, 0, rows * (d * 4.0 + 32));
+      HIP_TRY(launch_final(dt, s->h, rows, d, m->w("out_w"), m->b("out_b"), s->vact, st));
+    }
+  }
+  {
+    Scope sc(s, F3C_PROF_EULER, st, 0, (double)B * N * 128 + rows * 32.0);
+    const float dtf = (float)(t - t_next);
+    HIP_TRY(launch_euler(x, v_cache, s->vact, pos, act, B, N, dtf, v_prev, st));
+  }
+  s->cur = 1 - s->cur;
+  s->last_act = act;
+  return F3C_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* f3c_last_error(void) { return g_err.c_str(); }
+int f3c_version(void) { return 1; }
+
+int f3c_model_create(const f3c_model_cfg* cfg, f3c_model** out) {
+  if (!out) return fail(F3C_EINVAL, "out is NULL");
+  *out = nullptr;
+  int rc = validate_cfg(cfg);
+  if (rc) return rc;
+  f3c_model* m = new f3c_model();
+  m->cfg = *cfg;
+  m->N = cfg->grid * cfg->grid * cfg->grid;
+  m->d = cfg->width;
+  m->hd = cfg->width / cfg->heads;
+  m->dm = cfg->width * cfg->mlp_ratio;
+  m->L = cfg->depth;
+  m->dc = cfg->cond_width;
+  m->Nc = cfg->cond_tokens;
+  m->es = cfg->dtype == F3C_BF16 ? 2 : 4;
+  const int d = m->d, dc = m->dc, dm = m->dm, L = m->L;
+  auto add = [&](const std::string& n, int64_t r, int64_t c) { m->specs.push_back(Spec{n, r, c, c == 0}); };
+  add("in_w", d, 8);
+  add("in_b", d, 0);
+  add("pos", m->N, d);
+  add("t1_w", d, 256);
+  add("t1_b", d, 0);
+  add("t2_w", d, d);
+  add("t2_b", d, 0);
+  for (int l = 0; l < L; ++l) {
+    const std::string p = "blk" + std::to_string(l) + ".";
+    add(p + "mod_w", 6 * d, d);
+    add(p + "mod_b", 6 * d, 0);
+    add(p + "qkv_w", 3 * d, d);
+    add(p + "qkv_b", 3 * d, 0);
+    add(p + "o_w", d, d);
+    add(p + "o_b", d, 0);
+    add(p + "q_w", d, d);
+    add(p + "q_b", d, 0);
+    add(p + "kv_w", 2 * d, dc);
+    add(p + "kv_b", 2 * d, 0);
+    add(p + "co_w", d, d);
+    add(p + "co_b", d, 0);
+    add(p + "fc1_w", dm, d);
+    add(p + "fc1_b", dm, 0);
+    add(p + "fc2_w", d, dm);
+    add(p + "fc2_b", d, 0);
+  }
+  add("out_w", 8, d);
+  add("out_b", 8, 0);
+  // Layout: per-block modulation and cross-attention K/V weights are grouped
+  // across blocks so one GEMV / one GEMM serves all blocks.
+  size_t off = 0;
+  auto bytes_of = [&](const Spec& s) { return (size_t)s.numel() * (s.bias ? 4 : m->es); };
+  m->mod_w = off;
+  off = align256(off + (size_t)L * 6 * d * d * m->es);
+  m->mod_b = off;
+  off = align256(off + (size_t)L * 6 * d * 4);
+  m->kv_w = off;
+  off = align256(off + (size_t)L * 2 * d * dc * m->es);
+  m->kv_b = off;
+  off = align256(off + (size_t)L * 2 * d * 4);
+  for (auto& s : m->specs) {
+    const size_t dot = s.name.find('.');
+    if (dot != std::string::npos) {
+      const int l = std::stoi(s.name.substr(3, dot - 3));
+      const std::string k = s.name.substr(dot + 1);
+      if (k == "mod_w") { s.off = m->mod_w + (size_t)l * 6 * d * d * m->es; continue; }
+      if (k == "mod_b") { s.off = m->mod_b + (size_t)l * 6 * d * 4; continue; }
+      if (k == "kv_w") { s.off = m->kv_w + (size_t)l * 2 * d * dc * m->es; continue; }
+      if (k == "kv_b") { s.off = m->kv_b + (size_t)l * 2 * d * 4; continue; }
+    }
+    s.off = off;
+    off = align256(off + bytes_of(s));
+  }
+  m->wbytes = off;
+  *out = m;
+  return F3C_OK;
+}
+
+void f3c_model_destroy(f3c_model* m) { delete m; }
+
+int f3c_weight_count(const f3c_model* m, int32_t* n) {
+  if (!m || !n) return fail(F3C_EINVAL, "NULL argument");
+  *n = (int32_t)m->specs.size();
+  return F3C_OK;
+}
+
+int f3c_weight_info(const f3c_model* m, int32_t i, const char** name, int64_t* numel) {
+  if (!m || !name || !numel) return fail(F3C_EINVAL, "NULL argument");
+  if (i < 0 || i >= (int32_t)m->specs.size()) return fail(F3C_EINVAL, "weight index %d out of range", i);
+  *name = m->specs[i].name.c_str();
+  *numel = m->specs[i].numel();
+  return F3C_OK;
+}
+
+int f3c_model_weights_bytes(const f3c_model* m, size_t* bytes) {
+  if (!m || !bytes) return fail(F3C_EINVAL, "NULL argument");
+  *bytes = m->wbytes;
+  return F3C_OK;
+}
+
+int f3c_model_load_weights(f3c_model* m, void* weights_dev, size_t bytes, const float* const* host_f32, int32_t n) {
+  if (!m || !weights_dev || !host_f32) return fail(F3C_EINVAL, "NULL argument");
+  if ((uintptr_t)weights_dev & 255) return fail(F3C_EINVAL, "weights buffer must be 256-byte aligned");
+  if (bytes < m->wbytes) return fail(F3C_ENOMEM, "weights buffer %zu < %zu bytes", bytes, m->wbytes);
+  if (n != (int32_t)m->specs.size()) return fail(F3C_EINVAL, "expected %zu weight arrays, got %d", m->specs.size(), n);
+  for (int32_t i = 0; i < n; ++i)
+    if (!host_f32[i]) return fail(F3C_EINVAL, "weight %s is NULL", m->specs[i].name.c_str());
+  std::vector<char> stage;
+  char* dev = static_cast<char*>(weights_dev);
+  for (int32_t i = 0; i < n; ++i) {
+    const Spec& s = m->specs[i];
+    const int64_t ne = s.numel();
+    if (s.bias || m->es == 4) {
+      HIP_TRY(hipMemcpy(dev + s.off, host_f32[i], (size_t)ne * 4, hipMemcpyHostToDevice));
+    } else {
+      stage.resize((size_t)ne * 2);
+      uint16_t* o = reinterpret_cast<uint16_t*>(stage.data());
+      for (int64_t j = 0; j < ne; ++j) o[j] = f32_to_bf16_bits(host_f32[i][j]);
+      HIP_TRY(hipMemcpy(dev + s.off, stage.data(), (size_t)ne * 2, hipMemcpyHostToDevice));
+    }
+  }
+  m->wdev = dev;
+  m->loaded = true;
+  return F3C_OK;
+}
+
+double f3c_forward_flops(const f3c_model_cfg* c, int32_t n_tok, int32_t batch) {
+  if (!c) return 0.0;
+  return c->depth * block_flops(batch, n_tok, c->width, c->heads, c->cond_tokens, c->cond_width,
+                                (double)c->width * c->mlp_ratio);
+}
+
+int f3c_state_bytes(const f3c_model* m, int32_t batch, size_t* bytes) {
+  if (!m || !bytes) return fail(F3C_EINVAL, "NULL argument");
+  if (batch < 1 || batch > F3C_MAX_BATCH) return fail(F3C_EINVAL, "batch must be in 1..%d", F3C_MAX_BATCH);
+  const size_t R = (size_t)batch * m->N, d = m->d, es = m->es;
+  size_t t = 0;
+  t += 2 * align256(R * 32);                   // velocity cache pair
+  t += align256(R * d * 4);                    // h
+  t += 3 * align256(R * d * es);               // u, att, qc
+  t += align256(R * 3 * d * es);               // qkv
+  t += align256(R * m->dm * es);               // mlp hidden
+  t += align256(R * 32);                       // v_act
+  t += 3 * align256(R * 4);                    // idx, pos, score
+  t += align256((size_t)m->L * 6 * d * 4);     // mod
+  t += align256(2 * d * 4);                    // temb scratch
+  t += align256((size_t)batch * m->Nc * m->dc * es);              // condition tokens
+  t += align256((size_t)batch * m->Nc * 2 * m->L * d * es);       // cross K/V, all blocks
+  *bytes = t;
+  return F3C_OK;
+}
+
+int f3c_state_create(f3c_model* m, int32_t batch, void* state_dev, size_t bytes, f3c_stream stream,
+                     f3c_state** out) {
+  if (!m || !state_dev || !out) return fail(F3C_EINVAL, "NULL argument");
+  *out = nullptr;
+  size_t need = 0;
+  int rc = f3c_state_bytes(m, batch, &need);
+  if (rc) return rc;
+  if ((uintptr_t)state_dev & 255) return fail(F3C_EINVAL, "state buffer must be 256-byte aligned");
+  if (bytes < need) return fail(F3C_ENOMEM, "state buffer %zu < %zu bytes", bytes, need);
+  f3c_state* s = new f3c_state();
+  s->m = m;
+  s->B = batch;
+  s->dev = static_cast<char*>(state_dev);
+  s->bytes = bytes;
+  const size_t R = (size_t)batch * m->N, d = m->d, es = m->es;
+  char* p = s->dev;
+  auto take = [&](size_t n) { char* r = p; p += align256(n); return r; };
+  s->v[0] = (float*)take(R * 32);
+  s->v[1] = (float*)take(R * 32);
+  s->h = (float*)take(R * d * 4);
+  s->u = take(R * d * es);
+  s->att = take(R * d * es);
+  s->qc = take(R * d * es);
+  s->qkv = take(R * 3 * d * es);
+  s->hid = take(R * m->dm * es);
+  s->vact = (float*)take(R * 32);
+  s->idx = (int32_t*)take(R * 4);
+  s->pos = (int32_t*)take(R * 4);
+  s->score = (float*)take(R * 4);
+  s->mod = (float*)take((size_t)m->L * 6 * d * 4);
+  s->temb = (float*)take(2 * d * 4);
+  s->cond_t = take((size_t)batch * m->Nc * m->dc * es);
+  s->kv = take((size_t)batch * m->Nc * 2 * m->L * d * es);
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e = hipMemsetAsync(s->v[0], 0, R * 32, st);
+  if (e == hipSuccess) e = hipMemsetAsync(s->v[1], 0, R * 32, st);
+  if (e != hipSuccess) {
+    delete s;
+    return fail(F3C_EHIP, "zeroing caches: %s", hipGetErrorString(e));
+  }
+  *out = s;
+  return F3C_OK;
+}
+
+void f3c_state_destroy(f3c_state* s) {
+  if (!s) return;
+  for (auto& p : s->prof)
+    for (auto e : p.ev) (void)hipEventDestroy(e);
+  for (auto e : s->pool) (void)hipEventDestroy(e);
+  delete s;
+}
+
+int f3c_state_reset(f3c_state* s, f3c_stream stream) {
+  if (!s) return fail(F3C_EINVAL, "state is NULL");
+  const size_t R = (size_t)s->B * s->m->N;
+  HIP_TRY(hipMemsetAsync(s->v[0], 0, R * 32, (hipStream_t)stream));
+  HIP_TRY(hipMemsetAsync(s->v[1], 0, R * 32, (hipStream_t)stream));
+  s->cur = 0;
+  return F3C_OK;
+}
+
+int f3c_state_set_omega(f3c_state* s, float omega) {
+  if (!s) return fail(F3C_EINVAL, "state is NULL");
+  if (!(omega >= 0.0f && omega <= 1.0f)) return fail(F3C_EINVAL, "omega must be in [0, 1]");
+  s->omega = omega;
+  return F3C_OK;
+}
+
+int f3c_set_cond(f3c_state* s, const float* cond_dev, f3c_stream stream) {
+  int rc = check_state(s);
+  if (rc) return rc;
+  if (!cond_dev) return fail(F3C_EINVAL, "cond is NULL");
+  f3c_model* m = s->m;
+  hipStream_t st = (hipStream_t)stream;
+  const int rows = s->B * m->Nc, n = 2 * m->L * m->d;
+  Scope sc(s, F3C_PROF_COND, st, 2.0 * rows * n * m->dc, 0);
+  HIP_TRY(launch_convert(m->cfg.dtype, cond_dev, s->cond_t, (int64_t)rows * m->dc, st));
+  HIP_TRY(launch_gemm(m->cfg.dtype, EPI_STORE, rows, n, m->dc, s->cond_t, m->dc, m->wdev + m->kv_w, m->dc,
+                      (const float*)(m->wdev + m->kv_b), nullptr, s->kv, n, nullptr, 0, st));
+  s->cond_set = true;
+  return F3C_OK;
+}
+
+static int step_common(f3c_state* s, float* x, double t, double t_next, const int32_t* n_cache, f3c_stream stream) {
+  int rc = check_state(s);
+  if (rc) return rc;
+  if (!s->cond_set) return fail(F3C_ESTATE, "condition not set (call f3c_set_cond first)");
+  if (!x) return fail(F3C_EINVAL, "x is NULL");
+  if (!std::isfinite(t) || !std::isfinite(t_next) || !(t > t_next))
+    return fail(F3C_EINVAL, "need finite t > t_next (got %g, %g)", t, t_next);
+  if (n_cache)
+    for (int b = 0; b < s->B; ++b)
+      if (n_cache[b] < 0 || n_cache[b] > s->m->N)
+        return fail(F3C_EINVAL, "n_cache[%d] = %d outside [0, %d]", b, n_cache[b], s->m->N);
+  return run_step(s, x, t, t_next, n_cache, (hipStream_t)stream);
+}
+
+int f3c_full_step(f3c_state* s, float* x_dev, double t, double t_next, f3c_stream stream) {
+  return step_common(s, x_dev, t, t_next, nullptr, stream);
+}
+
+int f3c_cached_step(f3c_state* s, float* x_dev, double t, double t_next, const int32_t* n_cache_host,
+                    f3c_stream stream) {
+  if (!n_cache_host) return fail(F3C_EINVAL, "n_cache is NULL");
+  return step_common(s, x_dev, t, t_next, n_cache_host, stream);
+}
+
+int f3c_state_views(const f3c_state* s, float** v_cache, float** v_prev, int32_t** idx_active, int32_t** pos,
+                    float** v_act, float** mod, float** score, int32_t* act_off_host) {
+  if (!s) return fail(F3C_EINVAL, "state is NULL");
+  if (v_cache) *v_cache = s->v[s->cur];
+  if (v_prev) *v_prev = s->v[1 - s->cur];
+  if (idx_active) *idx_active = s->idx;
+  if (pos) *pos = s->pos;
+  if (v_act) *v_act = s->vact;
+  if (mod) *mod = s->mod;
+  if (score) *score = s->score;
+  if (act_off_host)
+    for (int b = 0; b <= s->B; ++b) act_off_host[b] = s->last_act.off[b];
+  return F3C_OK;
+}
+
+int f3c_state_record_scores(f3c_state* s, int32_t on) {
+  if (!s) return fail(F3C_EINVAL, "state is NULL");
+  s->record_scores = on != 0;
+  return F3C_OK;
+}
+
+int f3c_state_export(const f3c_state* s, float* host, size_t n_floats, f3c_stream stream) {
+  if (!s || !host) return fail(F3C_EINVAL, "NULL argument");
+  const size_t R = (size_t)s->B * s->m->N * 8;
+  if (n_floats < 2 * R) return fail(F3C_ENOMEM, "host buffer holds %zu < %zu floats", n_floats, 2 * R);
+  hipStream_t st = (hipStream_t)stream;
+  HIP_TRY(hipMemcpyAsync(host, s->v[s->cur], R * 4, hipMemcpyDeviceToHost, st));
+  HIP_TRY(hipMemcpyAsync(host + R, s->v[1 - s->cur], R * 4, hipMemcpyDeviceToHost, st));
+  HIP_TRY(hipStreamSynchronize(st));
+  return F3C_OK;
+}
+
+int f3c_state_import(f3c_state* s, const float* host, size_t n_floats, f3c_stream stream) {
+  if (!s || !host) return fail(F3C_EINVAL, "NULL argument");
+  const size_t R = (size_t)s->B * s->m->N * 8;
+  if (n_floats < 2 * R) return fail(F3C_ENOMEM, "host buffer holds %zu < %zu floats", n_floats, 2 * R);
+  hipStream_t st = (hipStream_t)stream;
+  HIP_TRY(hipMemcpyAsync(s->v[s->cur], host, R * 4, hipMemcpyHostToDevice, st));
+  HIP_TRY(hipMemcpyAsync(s->v[1 - s->cur], host + R, R * 4, hipMemcpyHostToDevice, st));
+  HIP_TRY(hipStreamSynchronize(st));
+  return F3C_OK;
+}
+
+int f3c_profile_enable(f3c_state* s, int32_t on) {
+  if (!s) return fail(F3C_EINVAL, "state is NULL");
+  s->profiling = on != 0;
+  return F3C_OK;
+}
+
+int f3c_profile_read(f3c_state* s, int32_t cls, int64_t* launches, double* ms, double* flops, double* bytes) {
+  if (!s) return fail(F3C_EINVAL, "state is NULL");
+  if (cls < 0 || cls >= F3C_PROF_CLASSES) return fail(F3C_EINVAL, "class %d out of range", cls);
+  Prof& p = s->prof[cls];
+  double total = 0;
+  for (size_t i = 0; i + 1 < p.ev.size(); i += 2) {
+    HIP_TRY(hipEventSynchronize(p.ev[i + 1]));
+    float t = 0;
+    HIP_TRY(hipEventElapsedTime(&t, p.ev[i], p.ev[i + 1]));
+    total += t;
+  }
+  if (launches) *launches = p.launches;
+  if (ms) *ms = total;
+  if (flops) *flops = p.flops;
+  if (bytes) *bytes = p.bytes;
+  return F3C_OK;
+}
+
+int f3c_profile_reset(f3c_state* s) {
+  if (!s) return fail(F3C_EINVAL, "state is NULL");
+  for (auto& p : s->prof) {
+    for (auto e : p.ev) {
+      (void)hipEventSynchronize(e);
+      s->pool.push_back(e);
+    }
+    p.ev.clear();
+    p.launches = 0;
+    p.flops = p.bytes = 0;
+  }
+  return F3C_OK;
+}
+
+// ------------------------------------------------------------ operator entries
+
+int f3c_op_select(int32_t batch, int32_t n_tokens, const float* v_cache, const float* v_prev, float omega,
+                  const int32_t* n_cache_host, int32_t* idx_active, int32_t* pos, float* score, f3c_stream stream) {
+  if (batch < 1 || batch > F3C_MAX_BATCH) return fail(F3C_EINVAL, "batch must be in 1..%d", F3C_MAX_BATCH);
+  if (n_tokens < 1 || n_tokens > F3C_MAX_TOKENS) return fail(F3C_EINVAL, "n_tokens must be in 1..%d", F3C_MAX_TOKENS);
+  if (!v_cache || !v_prev || !n_cache_host || !idx_active || !pos) return fail(F3C_EINVAL, "NULL argument");
+  if (!(omega >= 0.0f && omega <= 1.0f)) return fail(F3C_EINVAL, "omega must be in [0, 1]");
+  Segs quota{}, act{};
+  quota.B = act.B = batch;
+  for (int b = 0; b < batch; ++b) {
+    const int c = n_cache_host[b];
+    if (c < 0 || c > n_tokens) return fail(F3C_EINVAL, "n_cache[%d] = %d outside [0, %d]", b, c, n_tokens);
+    quota.off[b] = c;
+    act.off[b + 1] = act.off[b] + n_tokens - c;
+  }
+  HIP_TRY(launch_select(v_cache, v_prev, batch, n_tokens, omega, 1.0f - omega, quota, act, idx_active, pos, score,
+                        (hipStream_t)stream));
+  return F3C_OK;
+}
+
+int f3c_op_gemm(int32_t dtype, int32_t epilogue, int32_t M, int32_t N, int32_t K, const void* A, int32_t lda,
+                const void* W, int32_t ldw, const float* bias, const float* gate, void* out, int32_t ldo,
+                float* resid, int32_t ldr, f3c_stream stream) {
+  if (dtype != F3C_F32 && dtype != F3C_BF16) return fail(F3C_EINVAL, "bad dtype");
+  if (epilogue < 0 || epilogue > 2) return fail(F3C_EINVAL, "bad epilogue");
+  const int es = dtype == F3C_BF16 ? 2 : 4;
+  if (M < 0 || N <= 0 || K <= 0) return fail(F3C_EINVAL, "bad shape");
+  if (N % 128) return fail(F3C_EINVAL, "N must be a multiple of 128");
+  if ((K * es) % 128) return fail(F3C_EINVAL, "K must be a multiple of %d", 128 / es);
+  if (lda < K || ldw < K || (lda * es) % 16 || (ldw * es) % 16) return fail(F3C_EINVAL, "bad leading dims");
+  if (!A || !W || !bias) return fail(F3C_EINVAL, "NULL operand");
+  if (epilogue == 2 ? (!resid || ldr < N) : (!out || ldo < N)) return fail(F3C_EINVAL, "bad output");
+  HIP_TRY(launch_gemm(dtype, epilogue, M, N, K, A, lda, W, ldw, bias, gate, out, ldo, resid, ldr,
+                      (hipStream_t)stream));
+  return F3C_OK;
+}
+
+int f3c_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int32_t batch, const int32_t* q_off_host,
+                     const int32_t* k_off_host, const void* q, int32_t ldq, const void* k, int32_t ldk,
+                     const void* v, int32_t ldv, void* o, int32_t ldo, f3c_stream stream) {
+  if (dtype != F3C_F32 && dtype != F3C_BF16) return fail(F3C_EINVAL, "bad dtype");
+  if (head_dim != 32 && head_dim != 64) return fail(F3C_EINVAL, "head_dim must be 32 or 64");
+  if (heads < 1 || heads > 65535) return fail(F3C_EINVAL, "bad heads");
+  if (batch < 1 || batch > F3C_MAX_BATCH) return fail(F3C_EINVAL, "batch must be in 1..%d", F3C_MAX_BATCH);
+  if (!q_off_host || !k_off_host || !q || !k || !v || !o) return fail(F3C_EINVAL, "NULL argument");
+  const int es = dtype == F3C_BF16 ? 2 : 4, w = heads * head_dim;
+  if (ldq < w || ldk < w || ldv < w || ldo < w) return fail(F3C_EINVAL, "leading dims below heads*head_dim");
+  if ((ldq * es) % 16 || (ldk * es) % 16 || (ldv * es) % 16) return fail(F3C_EINVAL, "rows must be 16-byte aligned");
+  Segs qs{}, ks{};
+  qs.B = ks.B = batch;
+  for (int b = 0; b <= batch; ++b) {
+    qs.off[b] = q_off_host[b];
+    ks.off[b] = k_off_host[b];
+    if (b > 0 && (qs.off[b] < qs.off[b - 1] || ks.off[b] < ks.off[b - 1]))
+      return fail(F3C_EINVAL, "offsets must be non-decreasing");
+  }
+  if (qs.off[0] < 0 || ks.off[0] < 0) return fail(F3C_EINVAL, "negative offset");
+  for (int b = 0; b < batch; ++b)
+    if (qs.off[b + 1] > qs.off[b] && ks.off[b + 1] == ks.off[b])
+      return fail(F3C_EINVAL, "sample %d has queries but no keys", b);
+  HIP_TRY(launch_attention(dtype, heads, head_dim, qs, ks, q, ldq, k, ldk, v, ldv, o, ldo, (hipStream_t)stream));
+  return F3C_OK;
+}
+
+int f3c_op_ln_mod(int32_t dtype, int32_t rows, int32_t d, const float* h, const float* shift, const float* scale,
+                  void* out, f3c_stream stream) {
+  if (dtype != F3C_F32 && dtype != F3C_BF16) return fail(F3C_EINVAL, "bad dtype");
+  if (rows < 0 || !h || !out) return fail(F3C_EINVAL, "bad argument");
+  if (d != 128 && d != 256 && d != 512 && d != 1024 && d != 2048) return fail(F3C_EINVAL, "unsupported d %d", d);
+  if ((shift == nullptr) != (scale == nullptr)) return fail(F3C_EINVAL, "shift and scale go together");
+  HIP_TRY(launch_ln_mod(dtype, h, rows, d, shift, scale, out, (hipStream_t)stream));
+  return F3C_OK;
+}
+
+int f3c_op_modulation(const f3c_model* m, double t, float* mod_dev, float* scratch_dev, f3c_stream stream) {
+  if (!m || !mod_dev || !scratch_dev) return fail(F3C_EINVAL, "NULL argument");
+  if (!m->loaded) return fail(F3C_ESTATE, "weights not loaded");
+  if (!std::isfinite(t)) return fail(F3C_EINVAL, "t must be finite");
+  hipStream_t st = (hipStream_t)stream;
+  const int d = m->d, dt = m->cfg.dtype;
+  HIP_TRY(launch_gemv(dt, m->w("t1_w"), m->b("t1_b"), nullptr, t, GEMV_IN_TIMESTEP, 1, d, 256, scratch_dev, st));
+  HIP_TRY(launch_gemv(dt, m->w("t2_w"), m->b("t2_b"), scratch_dev, 0.0, GEMV_IN_PLAIN, 1, d, d, scratch_dev + d, st));
+  HIP_TRY(launch_gemv(dt, m->wdev + m->mod_w, (const float*)(m->wdev + m->mod_b), scratch_dev + d, 0.0,
+                      GEMV_IN_PLAIN, 0, 6 * m->L * d, d, mod_dev, st));
+  return F3C_OK;
+}
+
+// ------------------------------------------------------------ host schedules
+
+static double shift_time(double u, double eta) { return eta * u / (1.0 + (eta - 1.0) * u); }
+
+int f3c_time_grid(int32_t steps, double eta, double* out_host) {
+  if (steps < 1 || !out_host) return fail(F3C_EINVAL, "need steps >= 1 and an output array");
+  if (!(eta > 0.0) || !std::isfinite(eta)) return fail(F3C_EINVAL, "eta must be positive and finite");
+  for (int k = 0; k <= steps; ++k) out_host[k] = shift_time(1.0 - (double)k / steps, eta);
+  return F3C_OK;
+}
+
+int32_t f3c_ceil_ratio(int32_t steps, double rho) {
+  const double p = steps * rho;
+  return (int32_t)std::ceil(p - 1e-9 * (p > 1 ? p : 1));
+}
+
+int32_t f3c_pcsc_quota(int32_t k, int32_t n_tokens, double sigma, double mu, int32_t k_anchor, double gamma_up) {
+  const double bound = n_tokens - sigma * std::exp(mu * (k - k_anchor)) / gamma_up;
+  const double f = std::floor(bound);
+  if (!(f > 0)) return 0;
+  if (f > n_tokens) return n_tokens;
+  return (int32_t)f;
+}
+
+int32_t f3c_phase_quota(int32_t k, int32_t steps, int32_t n_tokens, int32_t n_cache_phase2, double rho_a,
+                        double rho_off, double xi, int32_t f_corr) {
+  if (k <= f3c_ceil_ratio(steps, rho_a)) return 0;
+  const int32_t k_off = f3c_ceil_ratio(steps, rho_off);
+  if (k < k_off) return n_cache_phase2;
+  const int32_t k_refine = k - k_off;
+  if (f_corr > 0 && (k_refine + 1) % f_corr == 0) return 0;
+  const double p = n_tokens * xi;
+  return (int32_t)std::floor(p + 1e-9 * (p > 1 ? p : 1));
+}
+
+}  // extern "C"

@@ -1,0 +1,287 @@
+// Row-wise and element-wise kernels of the cached step: active-token gather +
+// input embedding, LayerNorm with adaLN modulation, final LayerNorm + output
+// projection, merge + Euler + cache rotation, the timestep/modulation GEMVs
+// and dtype conversion. All are HBM/latency bound; one 64-wide wavefront owns a
+// row and lanes stride across the row so every load instruction is coalesced.
+#include "common.h"
+#include "kernels.h"
+
+namespace f3c {
+
+namespace {
+
+constexpr float kLnEps = 1e-6f;
+
+// ---------------------------------------------------------------- gather + embed
+// h[r][n] = sum_c x[b][i][c] * W_in[n][c] + b_in[n] + P[i][n]   (Sec. 4.2 index-based
+// selection: x_active = x[:, I_active, :], positions travel with the token).
+template <typename T, int NPL>
+__global__ __launch_bounds__(256) void k_embed(const float* __restrict__ x, int N, const int32_t* __restrict__ idx,
+                                               Segs act, const T* __restrict__ w_in,
+                                               const float* __restrict__ b_in, const T* __restrict__ ptab,
+                                               float* __restrict__ h) {
+  constexpr int D = NPL * 64;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  const int total = act.off[act.B];
+  if (row >= total) return;
+  const int b = find_segment(act.off, act.B, row);
+  const int i = idx ? idx[row] : row - act.off[b];
+  const float* xr = x + ((size_t)b * N + i) * 8;
+  float xv[8];
+#pragma unroll
+  for (int c = 0; c < 8; ++c) xv[c] = xr[c];
+  const T* pr = ptab + (size_t)i * D;
+  float* hr = h + (size_t)row * D;
+#pragma unroll
+  for (int j = 0; j < NPL; ++j) {
+    const int n = lane + 64 * j;
+    const T* w = w_in + (size_t)n * 8;
+    float acc = 0.0f;
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc += xv[c] * to_f32(w[c]);
+    hr[n] = acc + b_in[n] + to_f32(pr[n]);
+  }
+}
+
+// ------------------------------------------------------------- LayerNorm (+mod)
+template <int NPL>
+__device__ __forceinline__ void row_stats(const float (&v)[NPL], float& mean, float& rstd) {
+  constexpr int D = NPL * 64;
+  float s = 0.0f;
+#pragma unroll
+  for (int j = 0; j < NPL; ++j) s += v[j];
+  mean = wave_sum(s) * (1.0f / D);
+  float q = 0.0f;
+#pragma unroll
+  for (int j = 0; j < NPL; ++j) {
+    const float c = v[j] - mean;
+    q += c * c;
+  }
+  rstd = rsqrtf(wave_sum(q) * (1.0f / D) + kLnEps);
+}
+
+template <typename T, int NPL>
+__global__ __launch_bounds__(256) void k_ln_mod(const float* __restrict__ h, int rows,
+                                                const float* __restrict__ shift, const float* __restrict__ scale,
+                                                T* __restrict__ out) {
+  constexpr int D = NPL * 64;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= rows) return;
+  const float* hr = h + (size_t)row * D;
+  float v[NPL];
+#pragma unroll
+  for (int j = 0; j < NPL; ++j) v[j] = hr[lane + 64 * j];
+  float mean, rstd;
+  row_stats<NPL>(v, mean, rstd);
+  T* o = out + (size_t)row * D;
+#pragma unroll
+  for (int j = 0; j < NPL; ++j) {
+    const int n = lane + 64 * j;
+    float u = (v[j] - mean) * rstd;
+    if (scale) u = u * (1.0f + scale[n]) + shift[n];
+    o[n] = from_f32<T>(u);
+  }
+}
+
+// ------------------------------------------------------ final norm + projection
+template <typename T, int NPL>
+__global__ __launch_bounds__(256) void k_final(const float* __restrict__ h, int rows, const T* __restrict__ w_out,
+                                               const float* __restrict__ b_out, float* __restrict__ v_act) {
+  constexpr int D = NPL * 64;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= rows) return;
+  const float* hr = h + (size_t)row * D;
+  float v[NPL];
+#pragma unroll
+  for (int j = 0; j < NPL; ++j) v[j] = hr[lane + 64 * j];
+  float mean, rstd;
+  row_stats<NPL>(v, mean, rstd);
+  float acc[8];
+#pragma unroll
+  for (int c = 0; c < 8; ++c) acc[c] = 0.0f;
+#pragma unroll
+  for (int j = 0; j < NPL; ++j) {
+    const int n = lane + 64 * j;
+    const float u = (v[j] - mean) * rstd;
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc[c] += u * to_f32(w_out[(size_t)c * D + n]);
+  }
+#pragma unroll
+  for (int c = 0; c < 8; ++c) acc[c] = wave_sum(acc[c]);
+  if (lane < 8) {
+    float r = acc[0];
+#pragma unroll
+    for (int c = 1; c < 8; ++c) r = (lane == c) ? acc[c] : r;
+    v_act[(size_t)row * 8 + lane] = r + b_out[lane];
+  }
+}
+
+// ------------------------------------------------------ merge + Euler + rotate
+// Algorithm 1 state update: v = v_cache; v[I_active] = v_active; S <- S - (t - t') v;
+// the new v is written to the other half of the cache ping-pong pair.
+__global__ __launch_bounds__(256) void k_euler(float* __restrict__ x, const float* __restrict__ v_cache,
+                                               const float* __restrict__ v_act, const int32_t* __restrict__ pos,
+                                               Segs act, int B, int N, float dt, float* __restrict__ v_new) {
+#pragma clang fp contract(off)
+  const int64_t tok = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (tok >= (int64_t)B * N) return;
+  const int b = (int)(tok / N);
+  const int i = (int)(tok - (int64_t)b * N);
+  const int p = pos ? pos[tok] : act.off[b] + i;
+  const float4* src = reinterpret_cast<const float4*>(p >= 0 ? v_act + (size_t)p * 8 : v_cache + tok * 8);
+  const float4 v0 = src[0], v1 = src[1];
+  float4* xr = reinterpret_cast<float4*>(x + tok * 8);
+  float4 x0 = xr[0], x1 = xr[1];
+  x0.x = __fsub_rn(x0.x, __fmul_rn(dt, v0.x));
+  x0.y = __fsub_rn(x0.y, __fmul_rn(dt, v0.y));
+  x0.z = __fsub_rn(x0.z, __fmul_rn(dt, v0.z));
+  x0.w = __fsub_rn(x0.w, __fmul_rn(dt, v0.w));
+  x1.x = __fsub_rn(x1.x, __fmul_rn(dt, v1.x));
+  x1.y = __fsub_rn(x1.y, __fmul_rn(dt, v1.y));
+  x1.z = __fsub_rn(x1.z, __fmul_rn(dt, v1.z));
+  x1.w = __fsub_rn(x1.w, __fmul_rn(dt, v1.w));
+  xr[0] = x0;
+  xr[1] = x1;
+  float4* vn = reinterpret_cast<float4*>(v_new + tok * 8);
+  vn[0] = v0;
+  vn[1] = v1;
+}
+
+// ----------------------------------------------------------------------- GEMV
+// y[r] = W[r] . f(x) + b[r] (optionally SiLU(y)). The input vector is staged in
+// LDS once per workgroup (optionally through SiLU, or generated as the
+// sinusoidal timestep features [cos(1000 t f_j), sin(1000 t f_j)],
+// f_j = 10000^(-j/half), evaluated in fp64); each wavefront then streams 16
+// weight rows with 16-byte loads.
+constexpr int kGemvRowsPerWave = 16;
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_gemv(const T* __restrict__ W, const float* __restrict__ bias,
+                                              const float* __restrict__ x, double t, int in_mode, int out_silu,
+                                              int rows, int K, float* __restrict__ y) {
+  extern __shared__ float xs[];
+  for (int k = threadIdx.x; k < K; k += 256) {
+    float v;
+    if (in_mode == GEMV_IN_TIMESTEP) {
+      const int half = K / 2;
+      const int j = k < half ? k : k - half;
+      const double arg = 1000.0 * t * pow(10000.0, -(double)j / half);
+      v = (float)(k < half ? cos(arg) : sin(arg));
+    } else {
+      v = x[k];
+      if (in_mode == GEMV_IN_SILU) v = silu(v);
+    }
+    xs[k] = v;
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int row0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * kGemvRowsPerWave;
+  constexpr int V = 16 / sizeof(T);
+  for (int rr = 0; rr < kGemvRowsPerWave; ++rr) {
+    const int row = row0 + rr;
+    if (row >= rows) return;
+    const T* wr = W + (size_t)row * K;
+    float acc = 0.0f;
+    for (int k0 = lane * V; k0 < K; k0 += 64 * V) {
+      if constexpr (sizeof(T) == 2) {
+        const bf16x8 w = *reinterpret_cast<const bf16x8*>(wr + k0);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc += (float)w[e] * xs[k0 + e];
+      } else {
+        const float4 w = *reinterpret_cast<const float4*>(wr + k0);
+        acc += w.x * xs[k0] + w.y * xs[k0 + 1] + w.z * xs[k0 + 2] + w.w * xs[k0 + 3];
+      }
+    }
+    acc = wave_sum(acc);
+    if (lane == 0) {
+      float r = acc + bias[row];
+      y[row] = out_silu ? silu(r) : r;
+    }
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_convert(const float* __restrict__ src, T* __restrict__ dst, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    dst[i] = from_f32<T>(src[i]);
+}
+
+#define F3C_NPL_LAUNCH(d, KERNEL, T, grid, s, ...)                                        \
+  do {                                                                                     \
+    switch ((d) / 64) {                                                                    \
+      case 2: hipLaunchKernelGGL((KERNEL<T, 2>), grid, dim3(256), 0, s, __VA_ARGS__); break;   \
+      case 4: hipLaunchKernelGGL((KERNEL<T, 4>), grid, dim3(256), 0, s, __VA_ARGS__); break;   \
+      case 8: hipLaunchKernelGGL((KERNEL<T, 8>), grid, dim3(256), 0, s, __VA_ARGS__); break;   \
+      case 16: hipLaunchKernelGGL((KERNEL<T, 16>), grid, dim3(256), 0, s, __VA_ARGS__); break; \
+      case 32: hipLaunchKernelGGL((KERNEL<T, 32>), grid, dim3(256), 0, s, __VA_ARGS__); break; \
+      default: return hipErrorInvalidValue;                                                \
+    }                                                                                      \
+    return hipGetLastError();                                                              \
+  } while (0)
+
+}  // namespace
+
+hipError_t launch_embed(int dt, const float* x, int N, const int32_t* idx, const Segs& act, const void* w_in,
+                        const float* b_in, const void* pos_table, int d, float* h, hipStream_t s) {
+  const int rows = act.off[act.B];
+  if (rows == 0) return hipSuccess;
+  dim3 grid((rows + 3) / 4);
+  if (dt == DT_BF16)
+    F3C_NPL_LAUNCH(d, k_embed, bf16, grid, s, x, N, idx, act, (const bf16*)w_in, b_in, (const bf16*)pos_table, h);
+  F3C_NPL_LAUNCH(d, k_embed, float, grid, s, x, N, idx, act, (const float*)w_in, b_in, (const float*)pos_table, h);
+}
+
+hipError_t launch_ln_mod(int dt, const float* h, int rows, int d, const float* shift, const float* scale, void* out,
+                         hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  dim3 grid((rows + 3) / 4);
+  if (dt == DT_BF16) F3C_NPL_LAUNCH(d, k_ln_mod, bf16, grid, s, h, rows, shift, scale, (bf16*)out);
+  F3C_NPL_LAUNCH(d, k_ln_mod, float, grid, s, h, rows, shift, scale, (float*)out);
+}
+
+hipError_t launch_final(int dt, const float* h, int rows, int d, const void* w_out, const float* b_out,
+                        float* v_act, hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  dim3 grid((rows + 3) / 4);
+  if (dt == DT_BF16) F3C_NPL_LAUNCH(d, k_final, bf16, grid, s, h, rows, (const bf16*)w_out, b_out, v_act);
+  F3C_NPL_LAUNCH(d, k_final, float, grid, s, h, rows, (const float*)w_out, b_out, v_act);
+}
+
+hipError_t launch_euler(float* x, const float* v_cache, const float* v_act, const int32_t* pos, const Segs& act,
+                        int B, int N, float dt, float* v_new, hipStream_t s) {
+  const int64_t n = (int64_t)B * N;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_euler, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, x, v_cache, v_act, pos, act, B,
+                     N, dt, v_new);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemv(int dt, const void* W, const float* bias, const float* x, double t, int in_mode,
+                       int out_silu, int rows, int K, float* y, hipStream_t s) {
+  const int per_block = 4 * kGemvRowsPerWave;
+  dim3 grid((rows + per_block - 1) / per_block);
+  const size_t lds = (size_t)K * sizeof(float);
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL(k_gemv<bf16>, grid, dim3(256), lds, s, (const bf16*)W, bias, x, t, in_mode, out_silu, rows,
+                       K, y);
+  else
+    hipLaunchKernelGGL(k_gemv<float>, grid, dim3(256), lds, s, (const float*)W, bias, x, t, in_mode, out_silu,
+                       rows, K, y);
+  return hipGetLastError();
+}
+
+hipError_t launch_convert(int dt, const float* src, void* dst, int64_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const int64_t blocks = (n + 255) / 256;
+  dim3 grid((unsigned)(blocks < 65536 ? blocks : 65536));
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL(k_convert<bf16>, grid, dim3(256), 0, s, src, (bf16*)dst, n);
+  else
+    hipLaunchKernelGGL(k_convert<float>, grid, dim3(256), 0, s, src, (float*)dst, n);
+  return hipGetLastError();
+}
+
+}  // namespace f3c

@@ -1,0 +1,72 @@
+// Internal launchers for the gfx950 kernels. Host code in f3c.cpp validates
+// every shape before calling these; launchers only check launch errors.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace f3c {
+
+constexpr int kMaxBatch = 64;          // samples per step (segment tables travel by value)
+constexpr int kMaxTokens = 32768;      // tokens per sample handled by the one-workgroup selector
+
+// Segment table passed by value: sample b owns rows [off[b], off[b+1]).
+struct Segs {
+  int B;
+  int off[kMaxBatch + 1];
+};
+
+enum Dtype { DT_F32 = 0, DT_BF16 = 1 };
+enum Epilogue { EPI_STORE = 0, EPI_GELU = 1, EPI_RESID = 2 };
+
+// Stability score + lowest-score selection, one workgroup per sample.
+// v_cache, v_prev: f32 [B][N][8]. n_cache: per-sample cached counts (by value).
+// act: active-row offsets (by value). Writes idx_active[act.off[b] + r] (ascending
+// token index of the r-th active token), pos[b*N + i] (packed row or -1) and,
+// when score != nullptr, the float32 score of every token (only for c_b > 0).
+hipError_t launch_select(const float* v_cache, const float* v_prev, int B, int N, float w_a, float w_v,
+                         const Segs& n_cache, const Segs& act, int32_t* idx_active, int32_t* pos,
+                         float* score, hipStream_t s);
+
+// h[r][:] = x[b][i][:] W_in^T + b_in + P[i][:], i = idx_active[r] (identity when idx == nullptr).
+hipError_t launch_embed(int dt, const float* x, int N, const int32_t* idx, const Segs& act,
+                        const void* w_in, const float* b_in, const void* pos_table, int d, float* h,
+                        hipStream_t s);
+
+// out = LN(h) * (1 + scale) + shift, written as the model dtype; scale/shift may be null.
+hipError_t launch_ln_mod(int dt, const float* h, int rows, int d, const float* shift, const float* scale,
+                         void* out, hipStream_t s);
+
+// v_act[r][c] = LN(h[r]) . W_out[c] + b_out[c], c < 8 (f32 output).
+hipError_t launch_final(int dt, const float* h, int rows, int d, const void* w_out, const float* b_out,
+                        float* v_act, hipStream_t s);
+
+// Merge + Euler + rotate: v = (pos >= 0 ? v_act[pos] : v_cache); x -= dt * v; v_new = v.
+// pos == nullptr means every token active at row act.off[b] + i.
+hipError_t launch_euler(float* x, const float* v_cache, const float* v_act, const int32_t* pos,
+                        const Segs& act, int B, int N, float dt, float* v_new, hipStream_t s);
+
+// y[r] = W[r] . f(x) + b[r] (then SiLU when out_silu), f = identity / SiLU, or
+// x := the K sinusoidal features of t. K must be a multiple of 16 / sizeof(element).
+enum GemvIn { GEMV_IN_PLAIN = 0, GEMV_IN_SILU = 1, GEMV_IN_TIMESTEP = 2 };
+hipError_t launch_gemv(int dt, const void* W, const float* bias, const float* x, double t, int in_mode,
+                       int out_silu, int rows, int K, float* y, hipStream_t s);
+
+// Element type conversion f32 -> model dtype.
+hipError_t launch_convert(int dt, const float* src, void* dst, int64_t n, hipStream_t s);
+
+// C = A W^T + bias with an epilogue. A: [M][lda], W: [N][ldw] (model dtype),
+// bias f32 [N]. EPI_STORE / EPI_GELU write out[M][ldo] in the model dtype;
+// EPI_RESID does resid[m][n] += (gate ? gate[n] : 1) * value in f32.
+// Requires N % 128 == 0 and K % (128 / sizeof(element)) == 0.
+hipError_t launch_gemm(int dt, int epi, int M, int N, int K, const void* A, int lda, const void* W, int ldw,
+                       const float* bias, const float* gate, void* out, int ldo, float* resid, int ldr,
+                       hipStream_t s);
+
+// Varlen multi-head softmax attention. Queries of sample b are rows
+// [qs.off[b], qs.off[b+1]) of q; its keys/values are rows [ks.off[b], ks.off[b+1])
+// of k and v. Head h uses columns [h*hd, (h+1)*hd). Output rows match queries.
+hipError_t launch_attention(int dt, int heads, int hd, const Segs& qs, const Segs& ks, const void* q, int ldq,
+                            const void* k, int ldk, const void* v, int ldv, void* o, int ldo, hipStream_t s);
+
+}  // namespace f3c

@@ -1,0 +1,344 @@
+"""ctypes binding of the f3c C ABI (include/f3c.h).
+
+Argument marshalling only: every call forwards to libf3c.so, which runs every
+step of the cached sampler in HIP kernels. Device memory and streams come from
+PyTorch (``torch.empty(..., device="cuda")`` buffers and the current stream);
+nothing here computes any part of the method.
+
+If the library has not been built, ``lib()`` raises: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from typing import Dict, Optional, Sequence
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "lib", "libf3c.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "f3c.h")
+
+F3C_OK, F3C_EINVAL, F3C_ENOMEM, F3C_EHIP, F3C_ESTATE = 0, -1, -2, -3, -4
+F3C_F32, F3C_BF16 = 0, 1
+PROF_CLASSES = ["select", "embed", "mod", "ln", "gemm_qkv", "attn_self", "gemm_o", "gemm_q", "attn_cross",
+                "gemm_co", "gemm_fc1", "gemm_fc2", "final", "euler", "cond"]
+
+c_int, c_i64, c_f, c_d, c_sz, c_p = (ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double,
+                                     ctypes.c_size_t, ctypes.c_void_p)
+P_i32 = ctypes.POINTER(ctypes.c_int32)
+P_f = ctypes.POINTER(ctypes.c_float)
+P_d = ctypes.POINTER(ctypes.c_double)
+
+
+class F3CError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"f3c error {code}: {msg}")
+        self.code = code
+
+
+class ModelCfg(ctypes.Structure):
+    _fields_ = [(n, c_int) for n in ("grid", "in_ch", "width", "depth", "heads", "mlp_ratio", "cond_tokens",
+                                     "cond_width", "dtype")]
+
+
+_SIGS = {
+    "f3c_last_error": (ctypes.c_char_p, []),
+    "f3c_version": (c_int, []),
+    "f3c_model_create": (c_int, [ctypes.POINTER(ModelCfg), ctypes.POINTER(c_p)]),
+    "f3c_model_destroy": (None, [c_p]),
+    "f3c_weight_count": (c_int, [c_p, P_i32]),
+    "f3c_weight_info": (c_int, [c_p, c_int, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(c_i64)]),
+    "f3c_model_weights_bytes": (c_int, [c_p, ctypes.POINTER(c_sz)]),
+    "f3c_model_load_weights": (c_int, [c_p, c_p, c_sz, ctypes.POINTER(P_f), c_int]),
+    "f3c_forward_flops": (c_d, [ctypes.POINTER(ModelCfg), c_int, c_int]),
+    "f3c_state_bytes": (c_int, [c_p, c_int, ctypes.POINTER(c_sz)]),
+    "f3c_state_create": (c_int, [c_p, c_int, c_p, c_sz, c_p, ctypes.POINTER(c_p)]),
+    "f3c_state_destroy": (None, [c_p]),
+    "f3c_state_reset": (c_int, [c_p, c_p]),
+    "f3c_state_set_omega": (c_int, [c_p, c_f]),
+    "f3c_set_cond": (c_int, [c_p, c_p, c_p]),
+    "f3c_full_step": (c_int, [c_p, c_p, c_d, c_d, c_p]),
+    "f3c_cached_step": (c_int, [c_p, c_p, c_d, c_d, P_i32, c_p]),
+    "f3c_state_views": (c_int, [c_p] + [ctypes.POINTER(c_p)] * 7 + [P_i32]),
+    "f3c_state_record_scores": (c_int, [c_p, c_int]),
+    "f3c_state_export": (c_int, [c_p, P_f, c_sz, c_p]),
+    "f3c_state_import": (c_int, [c_p, P_f, c_sz, c_p]),
+    "f3c_profile_enable": (c_int, [c_p, c_int]),
+    "f3c_profile_read": (c_int, [c_p, c_int, ctypes.POINTER(c_i64), P_d, P_d, P_d]),
+    "f3c_profile_reset": (c_int, [c_p]),
+    "f3c_op_select": (c_int, [c_int, c_int, c_p, c_p, c_f, P_i32, c_p, c_p, c_p, c_p]),
+    "f3c_op_gemm": (c_int, [c_int, c_int, c_int, c_int, c_int, c_p, c_int, c_p, c_int, c_p, c_p, c_p, c_int, c_p,
+                            c_int, c_p]),
+    "f3c_op_attention": (c_int, [c_int, c_int, c_int, c_int, P_i32, P_i32, c_p, c_int, c_p, c_int, c_p, c_int, c_p,
+                                 c_int, c_p]),
+    "f3c_op_ln_mod": (c_int, [c_int, c_int, c_int, c_p, c_p, c_p, c_p, c_p]),
+    "f3c_op_modulation": (c_int, [c_p, c_d, c_p, c_p, c_p]),
+    "f3c_time_grid": (c_int, [c_int, c_d, P_d]),
+    "f3c_ceil_ratio": (c_int, [c_int, c_d]),
+    "f3c_pcsc_quota": (c_int, [c_int, c_int, c_d, c_d, c_int, c_d]),
+    "f3c_phase_quota": (c_int, [c_int, c_int, c_int, c_int, c_d, c_d, c_d, c_int]),
+}
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libf3c.so (built in-tree by build.py); raise if it is missing."""
+    global _lib
+    if _lib is None:
+        # PyTorch ships its own HIP runtime (same soname). Importing it first makes
+        # libf3c.so bind to that runtime, so streams and allocations are shared
+        # by one runtime instance in the process.
+        import torch  # noqa: F401
+        if not os.path.exists(LIB_PATH):
+            raise F3CError(F3C_ESTATE, f"{LIB_PATH} not built; run paper_2511_22533_amd.build")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def header_symbols() -> list:
+    """Function names declared in include/f3c.h."""
+    with open(HEADER) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(f3c_[a-z_0-9]+)\s*\(", text)))
+
+
+def check(rc: int) -> None:
+    if rc != F3C_OK:
+        raise F3CError(rc, lib().f3c_last_error().decode())
+
+
+def _i32(a: Sequence[int]):
+    arr = (ctypes.c_int32 * len(a))(*[int(x) for x in a])
+    return arr
+
+
+def model_cfg(cfg) -> ModelCfg:
+    """ModelCfg from a synth.ModelConfig."""
+    return ModelCfg(cfg.grid, cfg.in_ch, cfg.width, cfg.depth, cfg.heads, cfg.mlp_ratio, cfg.cond_tokens,
+                    cfg.cond_width, F3C_BF16 if cfg.dtype == "bf16" else F3C_F32)
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return int(stream)
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+# ---------------------------------------------------------------- host schedules
+
+def time_grid(steps: int, eta: float) -> np.ndarray:
+    out = (ctypes.c_double * (steps + 1))()
+    check(lib().f3c_time_grid(steps, eta, out))
+    return np.array(out[:], dtype=np.float64)
+
+
+def ceil_ratio(steps: int, rho: float) -> int:
+    return int(lib().f3c_ceil_ratio(steps, rho))
+
+
+def pcsc_quota(k, n_tokens, sigma, mu, k_anchor, gamma_up) -> int:
+    return int(lib().f3c_pcsc_quota(k, n_tokens, sigma, mu, k_anchor, gamma_up))
+
+
+def phase_quota(k, steps, n_tokens, n_cache_phase2, rho_a=0.2, rho_off=0.75, xi=0.7, f_corr=3) -> int:
+    return int(lib().f3c_phase_quota(k, steps, n_tokens, n_cache_phase2, rho_a, rho_off, xi, f_corr))
+
+
+def forward_flops(cfg, n_tok: int, batch: int = 1) -> float:
+    c = model_cfg(cfg)
+    return float(lib().f3c_forward_flops(ctypes.byref(c), n_tok, batch))
+
+
+# ---------------------------------------------------------------- model / state
+
+class Model:
+    """A model handle plus its torch-allocated weight buffer."""
+
+    def __init__(self, cfg):
+        self.cfg = cfg
+        self.c = model_cfg(cfg)
+        h = c_p()
+        check(lib().f3c_model_create(ctypes.byref(self.c), ctypes.byref(h)))
+        self.h = h
+        self.wbuf = None
+
+    def weight_names(self):
+        n = c_int()
+        check(lib().f3c_weight_count(self.h, ctypes.byref(n)))
+        out = []
+        for i in range(n.value):
+            name, numel = ctypes.c_char_p(), c_i64()
+            check(lib().f3c_weight_info(self.h, i, ctypes.byref(name), ctypes.byref(numel)))
+            out.append((name.value.decode(), numel.value))
+        return out
+
+    def weights_bytes(self) -> int:
+        b = c_sz()
+        check(lib().f3c_model_weights_bytes(self.h, ctypes.byref(b)))
+        return b.value
+
+    def load(self, weights: Dict[str, np.ndarray]):
+        import torch
+        names = self.weight_names()
+        arrs = []
+        for name, numel in names:
+            a = np.ascontiguousarray(weights[name], dtype=np.float32).reshape(-1)
+            if a.size != numel:
+                raise F3CError(F3C_EINVAL, f"{name}: expected {numel} values, got {a.size}")
+            arrs.append(a)
+        self.wbuf = torch.empty(self.weights_bytes(), dtype=torch.uint8, device="cuda")
+        ptrs = (P_f * len(arrs))(*[a.ctypes.data_as(P_f) for a in arrs])
+        check(lib().f3c_model_load_weights(self.h, self.wbuf.data_ptr(), self.wbuf.numel(), ptrs, len(arrs)))
+        return self
+
+    def modulation(self, t: float, stream=None):
+        import torch
+        mod = torch.empty(self.cfg.depth * 6 * self.cfg.width, dtype=torch.float32, device="cuda")
+        scratch = torch.empty(2 * self.cfg.width, dtype=torch.float32, device="cuda")
+        check(lib().f3c_op_modulation(self.h, t, mod.data_ptr(), scratch.data_ptr(), _stream(stream)))
+        return mod.view(self.cfg.depth, 6, self.cfg.width)
+
+    def __del__(self):
+        if getattr(self, "h", None) and _lib is not None:
+            _lib.f3c_model_destroy(self.h)
+            self.h = None
+
+
+class State:
+    """A sampler state (velocity caches, activations, condition K/V) of one model."""
+
+    def __init__(self, model: Model, batch: int, stream=None):
+        import torch
+        self.model, self.batch = model, batch
+        b = c_sz()
+        check(lib().f3c_state_bytes(model.h, batch, ctypes.byref(b)))
+        self.buf = torch.empty(b.value, dtype=torch.uint8, device="cuda")
+        h = c_p()
+        check(lib().f3c_state_create(model.h, batch, self.buf.data_ptr(), self.buf.numel(), _stream(stream),
+                                     ctypes.byref(h)))
+        self.h = h
+
+    def reset(self, stream=None):
+        check(lib().f3c_state_reset(self.h, _stream(stream)))
+
+    def set_omega(self, omega: float):
+        check(lib().f3c_state_set_omega(self.h, omega))
+
+    def set_cond(self, cond, stream=None):
+        check(lib().f3c_set_cond(self.h, cond.data_ptr(), _stream(stream)))
+
+    def full_step(self, x, t: float, t_next: float, stream=None):
+        check(lib().f3c_full_step(self.h, x.data_ptr(), t, t_next, _stream(stream)))
+
+    def cached_step(self, x, t: float, t_next: float, n_cache: Sequence[int], stream=None):
+        check(lib().f3c_cached_step(self.h, x.data_ptr(), t, t_next, _i32(n_cache), _stream(stream)))
+
+    def record_scores(self, on: bool):
+        check(lib().f3c_state_record_scores(self.h, int(on)))
+
+    def views(self):
+        """Device pointers of the caches/selection and the last step's active offsets."""
+        ps = [c_p() for _ in range(7)]
+        off = (ctypes.c_int32 * (self.batch + 1))()
+        check(lib().f3c_state_views(self.h, *[ctypes.byref(p) for p in ps], off))
+        keys = ["v_cache", "v_prev", "idx_active", "pos", "v_act", "mod", "score"]
+        out = {k: p.value for k, p in zip(keys, ps)}
+        out["act_off"] = list(off)
+        return out
+
+    def tensors(self):
+        """Zero-copy torch views of the state's device buffers (caches, selection, v_act, mod, score)."""
+        import torch
+        v = self.views()
+        cfg, B = self.model.cfg, self.batch
+        N = cfg.tokens
+        rows = v["act_off"][-1]
+        base = self.buf.data_ptr()
+
+        def view(ptr, n, dtype, shape):
+            off = ptr - base
+            nbytes = n * torch.empty((), dtype=dtype).element_size()
+            return self.buf[off:off + nbytes].view(dtype).view(shape)
+
+        return {
+            "v_cache": view(v["v_cache"], B * N * 8, torch.float32, (B, N, 8)),
+            "v_prev": view(v["v_prev"], B * N * 8, torch.float32, (B, N, 8)),
+            "idx_active": view(v["idx_active"], rows, torch.int32, (rows,)),
+            "pos": view(v["pos"], B * N, torch.int32, (B, N)),
+            "v_act": view(v["v_act"], rows * 8, torch.float32, (rows, 8)),
+            "mod": view(v["mod"], cfg.depth * 6 * cfg.width, torch.float32, (cfg.depth, 6, cfg.width)),
+            "score": view(v["score"], B * N, torch.float32, (B, N)),
+            "act_off": v["act_off"],
+        }
+
+    def export(self, stream=None) -> np.ndarray:
+        n = 2 * self.batch * self.model.cfg.tokens * 8
+        host = np.empty(n, np.float32)
+        check(lib().f3c_state_export(self.h, host.ctypes.data_as(P_f), n, _stream(stream)))
+        return host
+
+    def import_(self, host: np.ndarray, stream=None):
+        host = np.ascontiguousarray(host, dtype=np.float32)
+        check(lib().f3c_state_import(self.h, host.ctypes.data_as(P_f), host.size, _stream(stream)))
+
+    def profile(self, on: bool):
+        check(lib().f3c_profile_enable(self.h, int(on)))
+
+    def profile_reset(self):
+        check(lib().f3c_profile_reset(self.h))
+
+    def profile_read(self) -> Dict[str, dict]:
+        out = {}
+        for i, name in enumerate(PROF_CLASSES):
+            n, ms, fl, by = c_i64(), c_d(), c_d(), c_d()
+            check(lib().f3c_profile_read(self.h, i, ctypes.byref(n), ctypes.byref(ms), ctypes.byref(fl),
+                                         ctypes.byref(by)))
+            out[name] = {"launches": n.value, "ms": ms.value, "flops": fl.value, "bytes": by.value}
+        return out
+
+    def __del__(self):
+        if getattr(self, "h", None) and _lib is not None:
+            _lib.f3c_state_destroy(self.h)
+            self.h = None
+
+
+# ---------------------------------------------------------------- operator calls
+
+def op_select(v_cache, v_prev, omega: float, n_cache: Sequence[int], idx_active, pos, score=None, stream=None):
+    B, N = v_cache.shape[0], v_cache.shape[1]
+    check(lib().f3c_op_select(B, N, v_cache.data_ptr(), v_prev.data_ptr(), omega, _i32(n_cache),
+                              idx_active.data_ptr(), pos.data_ptr(), _ptr(score), _stream(stream)))
+
+
+def op_gemm(dtype: int, epilogue: int, A, W, bias, out=None, resid=None, gate=None, stream=None):
+    M, K = A.shape
+    N = W.shape[0]
+    check(lib().f3c_op_gemm(dtype, epilogue, M, N, K, A.data_ptr(), A.stride(0), W.data_ptr(), W.stride(0),
+                            bias.data_ptr(), _ptr(gate), _ptr(out), out.stride(0) if out is not None else 0,
+                            _ptr(resid), resid.stride(0) if resid is not None else 0, _stream(stream)))
+
+
+def op_attention(dtype: int, heads: int, head_dim: int, q_off, k_off, q, k, v, o, stream=None):
+    B = len(q_off) - 1
+    check(lib().f3c_op_attention(dtype, heads, head_dim, B, _i32(q_off), _i32(k_off), q.data_ptr(), q.stride(0),
+                                 k.data_ptr(), k.stride(0), v.data_ptr(), v.stride(0), o.data_ptr(), o.stride(0),
+                                 _stream(stream)))
+
+
+def op_ln_mod(dtype: int, h, out, shift=None, scale=None, stream=None):
+    rows, d = h.shape
+    check(lib().f3c_op_ln_mod(dtype, rows, d, h.data_ptr(), _ptr(shift), _ptr(scale), out.data_ptr(),
+                              _stream(stream)))

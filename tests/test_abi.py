@@ -1,0 +1,131 @@
+"""Host-side checks of the C ABI (no GPU needed).
+
+* the library loads and exports every function include/f3c.h declares;
+* the canonical weight list matches the seeded generator's parameter list;
+* argument validation rejects bad shapes before any device work;
+* the host schedules (Eq. S1 time grid, ceil ratios, Algorithm 1 phase rule,
+  Eqs. 4-5 quota) and the FLOPs model agree with the oracle's restatement.
+"""
+import ctypes
+import math
+import subprocess
+
+import numpy as np
+import pytest
+
+from oracle import flops as oflops
+from oracle import schedule as osched
+from paper_2511_22533_amd import f3c, synth
+
+
+@pytest.fixture(scope="module")
+def L():
+    return f3c.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    declared = f3c.header_symbols()
+    assert len(declared) >= 30
+    out = subprocess.run(["nm", "-D", "--defined-only", f3c.LIB_PATH], capture_output=True, text=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if " T " in line}
+    missing = [s for s in declared if s not in exported]
+    assert not missing, missing
+    for s in declared:
+        assert hasattr(L, s)
+    assert set(f3c._SIGS) == set(declared)
+
+
+@pytest.mark.parametrize("wname", sorted(synth.WORKLOADS))
+def test_weight_list_matches_generator(wname):
+    cfg = synth.WORKLOADS[wname].model
+    m = f3c.Model(cfg)
+    got = m.weight_names()
+    want = [(n, int(np.prod(s))) for n, s in synth.weight_specs(cfg)]
+    assert got == want
+
+
+def _cfg(**kw):
+    base = dict(grid=8, width=128, depth=2, heads=4, cond_tokens=64, cond_width=128, dtype="f32")
+    base.update(kw)
+    return synth.ModelConfig(**base)
+
+
+@pytest.mark.parametrize("kw,msg", [
+    (dict(width=96, heads=3), "multiple of 128"),
+    (dict(heads=8), "head_dim"),
+    (dict(grid=33), "exceeds"),
+    (dict(cond_width=100), "cond_width"),
+    (dict(depth=0), "depth"),
+    (dict(in_ch=4), "in_ch"),
+    (dict(width=384, heads=6), "power of two"),
+])
+def test_model_create_rejects_bad_shapes(kw, msg):
+    with pytest.raises(f3c.F3CError) as e:
+        f3c.Model(_cfg(**kw))
+    assert e.value.code == f3c.F3C_EINVAL and msg in str(e.value)
+
+
+def test_state_bytes_and_batch_limits(L):
+    m = f3c.Model(synth.TRELLIS16)
+    b = ctypes.c_size_t()
+    assert L.f3c_state_bytes(m.h, 1, ctypes.byref(b)) == 0 and b.value > 0
+    b4 = ctypes.c_size_t()
+    assert L.f3c_state_bytes(m.h, 4, ctypes.byref(b4)) == 0 and b4.value > 3 * b.value
+    assert L.f3c_state_bytes(m.h, 0, ctypes.byref(b)) == f3c.F3C_EINVAL
+    assert L.f3c_state_bytes(m.h, 65, ctypes.byref(b)) == f3c.F3C_EINVAL
+
+
+def test_steps_need_loaded_weights_and_valid_quota(L):
+    # state creation needs device memory; the checks below fail before touching it
+    assert L.f3c_full_step(None, None, 1.0, 0.5, None) == f3c.F3C_EINVAL
+    assert L.f3c_cached_step(None, None, 1.0, 0.5, None, None) == f3c.F3C_EINVAL
+
+
+def test_op_entry_validation_is_host_side(L):
+    q = f3c._i32([0, 5])
+    assert L.f3c_op_select(0, 512, 1, 1, 0.7, q, 1, 1, None, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_select(1, 512, 1, 1, 1.5, q, 1, 1, None, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_select(1, 4, 1, 1, 0.7, f3c._i32([5]), 1, 1, None, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_select(1, 40000, 1, 1, 0.7, f3c._i32([5]), 1, 1, None, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_gemm(1, 0, 16, 100, 64, 1, 64, 1, 64, 1, None, 1, 100, None, 0, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_gemm(1, 0, 16, 128, 40, 1, 40, 1, 40, 1, None, 1, 128, None, 0, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_attention(1, 4, 48, 1, q, q, 1, 192, 1, 192, 1, 192, 1, 192, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_attention(1, 4, 64, 1, f3c._i32([0, 3]), f3c._i32([0, 0]), 1, 256, 1, 256, 1, 256, 1, 256,
+                              None) == f3c.F3C_EINVAL
+    assert L.f3c_op_ln_mod(1, 4, 96, 1, None, None, 1, None) == f3c.F3C_EINVAL
+    assert b"unsupported d" in L.f3c_last_error()
+
+
+@pytest.mark.parametrize("steps,eta", [(10, 1.0), (25, 3.0), (25, 2.0), (50, 1.5)])
+def test_time_grid_matches_oracle_bitwise(steps, eta):
+    got = f3c.time_grid(steps, eta)
+    want = np.array(osched.time_grid(steps, eta))
+    assert np.array_equal(got, want)
+
+
+def test_ceil_ratio_and_phase_rule_match_oracle():
+    for T in (10, 20, 25, 40, 50):
+        for rho in (0.1, 0.2, 0.25, 0.3, 0.5, 0.6, 0.7, 0.75, 0.8):
+            assert f3c.ceil_ratio(T, rho) == osched.ceil_ratio(T, rho)
+    for T in (10, 25):
+        for f_corr in (0, 1, 2, 3, 4):
+            for xi in (0.7, 0.8, 0.9):
+                for k in range(1, T + 1):
+                    assert f3c.phase_quota(k, T, 4096, 1234, 0.2, 0.75, xi, f_corr) == \
+                        osched.phase_quota(k, T, 4096, 1234, 0.2, 0.75, xi, f_corr)
+
+
+def test_pcsc_quota_matches_oracle():
+    for N in (512, 4096, 32768):
+        for sigma in (0.0, 100.0, 6400.0, 2e5, 1e9):
+            for mu in (-0.7, -0.07, -0.007):
+                for k in range(5, 26):
+                    assert f3c.pcsc_quota(k, N, sigma, mu, 5, 64.0) == osched.pcsc_quota(k, N, sigma, mu, 5, 64.0)
+
+
+@pytest.mark.parametrize("wname", sorted(synth.WORKLOADS))
+def test_forward_flops_matches_oracle(wname):
+    cfg = synth.WORKLOADS[wname].model
+    for n in (0, 1, 820, cfg.tokens):
+        for B in (1, 4):
+            assert math.isclose(f3c.forward_flops(cfg, n, B), oflops.forward_flops(cfg, n, B), rel_tol=1e-12)

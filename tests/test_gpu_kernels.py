@@ -1,0 +1,244 @@
+"""GPU parity of each kernel of the step, through the C ABI, against the oracle.
+
+* scoring + selection: bit-exact scores, index sets and position map (Eqs. 2,
+  6, 7; Algorithm 1 SSC), including ties, NaN, quota 0 / N and ragged batches,
+  up to 32768 tokens per sample;
+* projections (MFMA GEMM, each epilogue) and attention (self, ragged varlen,
+  cross with a non-tile-multiple key count) against float64 on the same
+  bf16-rounded operands; bf16 bound 2e-2 max-rel, f32 bound 1e-4;
+* LayerNorm/modulation and the timestep modulation path.
+"""
+import numpy as np
+import pytest
+
+from helpers import bf16_round, max_rel, oracle_selection, say, to_dev
+from oracle import dit, ssc
+from paper_2511_22533_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    from paper_2511_22533_amd import f3c
+    f3c.lib()
+    return t
+
+
+def _run_select(torch, vc, vp, n_cache, omega):
+    from paper_2511_22533_amd import f3c
+    B, N = vc.shape[:2]
+    total = int(sum(N - c for c in n_cache))
+    d_vc, d_vp = to_dev(vc), to_dev(vp)
+    idx = torch.full((max(total, 1),), -7, dtype=torch.int32, device="cuda")
+    pos = torch.full((B, N), -7, dtype=torch.int32, device="cuda")
+    score = torch.full((B, N), float("nan"), dtype=torch.float32, device="cuda")
+    f3c.op_select(d_vc, d_vp, omega, n_cache, idx, pos, score)
+    torch.cuda.synchronize()
+    return idx.cpu().numpy()[:total], pos.cpu().numpy(), score.cpu().numpy()
+
+
+def _check_select(torch, vc, vp, n_cache, omega=0.7):
+    B, N = vc.shape[:2]
+    idx, pos, score = _run_select(torch, vc, vp, n_cache, omega)
+    ref = oracle_selection(vc, vp, n_cache, omega)
+    row = 0
+    for b in range(B):
+        s_ref, active = ref[b]
+        n = len(active)
+        assert n == N - n_cache[b]
+        assert np.array_equal(idx[row:row + n], active), f"sample {b}"
+        want_pos = np.full(N, -1, np.int64)
+        want_pos[active] = row + np.arange(n)
+        assert np.array_equal(pos[b], want_pos), f"sample {b}"
+        if s_ref is not None:
+            assert np.array_equal(score[b].view(np.uint32), s_ref.view(np.uint32)), f"scores sample {b}"
+        row += n
+
+
+@pytest.mark.parametrize("B,N", [(1, 512), (1, 4096), (4, 4096), (1, 32768), (3, 1000), (2, 1)])
+def test_select_bit_exact_random(torch, B, N):
+    rng = np.random.default_rng(N + B)
+    vc = rng.standard_normal((B, N, 8)).astype(np.float32)
+    vp = (vc + 0.1 * rng.standard_normal((B, N, 8))).astype(np.float32)
+    for quotas in ([0] * B, [N] * B, [1] * B, [N - 1] * B,
+                   [int(q) for q in rng.integers(0, N + 1, size=B)],
+                   [int(N * f) for f in np.linspace(0.4, 0.85, B)]):
+        say("select", B, N, quotas)
+        _check_select(torch, vc, vp, quotas)
+
+
+@pytest.mark.parametrize("omega", [0.0, 0.3, 0.7, 1.0])
+def test_select_ties_and_sticky_cache(torch, omega):
+    rng = np.random.default_rng(11)
+    B, N = 2, 4096
+    vc = (rng.integers(-2, 3, size=(B, N, 8)) * 0.5).astype(np.float32)   # many equal scores
+    vp = vc.copy()
+    moved = rng.random((B, N)) < 0.3
+    vp[moved] += 0.5                                                      # A = 0 for the rest
+    say("select ties", omega)
+    _check_select(torch, vc, vp, [1000, 3000], omega)
+
+
+def test_select_degenerate_and_nan(torch):
+    B, N = 3, 2048
+    vc = np.ones((B, N, 8), np.float32)
+    vp = np.ones((B, N, 8), np.float32)             # max == min for both terms
+    rng = np.random.default_rng(3)
+    vc[1] = rng.standard_normal((N, 8)).astype(np.float32)
+    vp[1] = rng.standard_normal((N, 8)).astype(np.float32)
+    vc[1, 17, 3] = np.nan
+    vc[1, 900, :] = np.inf
+    vc[2] = rng.standard_normal((N, 8)).astype(np.float32)
+    vp[2] = vc[2]
+    say("select degenerate/nan")
+    _check_select(torch, vc, vp, [100, 1500, 2047])
+
+
+def _gemm_case(torch, dt, epi, M, N, K, seed):
+    from paper_2511_22533_amd import f3c
+    rng = np.random.default_rng(seed)
+    A = rng.standard_normal((M, K)).astype(np.float32)
+    W = (0.05 * rng.standard_normal((N, K))).astype(np.float32)
+    bias = rng.standard_normal(N).astype(np.float32)
+    gate = rng.standard_normal(N).astype(np.float32)
+    if dt == f3c.F3C_BF16:
+        A, W = bf16_round(A), bf16_round(W)
+        tdt = torch.bfloat16
+    else:
+        tdt = torch.float32
+    ref = A.astype(np.float64) @ W.astype(np.float64).T + bias
+    dA, dW, db, dg = to_dev(A, tdt), to_dev(W, tdt), to_dev(bias), to_dev(gate)
+    say("gemm", dt, epi, M, N, K)
+    if epi == 2:
+        r0 = rng.standard_normal((M, N)).astype(np.float32)
+        dr = to_dev(r0)
+        f3c.op_gemm(dt, 2, dA, dW, db, resid=dr, gate=dg)
+        torch.cuda.synchronize()
+        got = dr.cpu().numpy().astype(np.float64) - r0
+        want = gate * ref
+    else:
+        out = torch.empty((M, N), dtype=tdt, device="cuda")
+        f3c.op_gemm(dt, epi, dA, dW, db, out=out)
+        torch.cuda.synchronize()
+        got = out.float().cpu().numpy()
+        want = dit.gelu_tanh(ref) if epi == 1 else ref
+    return got, want
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 128, 64), (37, 384, 128), (128, 1024, 1024), (820, 3072, 1024),
+                                   (4096, 1024, 4096), (2057, 4096, 1024)])
+@pytest.mark.parametrize("epi", [0, 1, 2])
+def test_gemm_bf16(torch, M, N, K, epi):
+    from paper_2511_22533_amd import f3c
+    got, want = _gemm_case(torch, f3c.F3C_BF16, epi, M, N, K, seed=M * 7 + N + epi)
+    assert max_rel(got, want) < 1e-2
+
+
+@pytest.mark.parametrize("M,N,K", [(1, 128, 32), (300, 384, 128), (513, 512, 128)])
+@pytest.mark.parametrize("epi", [0, 1, 2])
+def test_gemm_f32(torch, M, N, K, epi):
+    from paper_2511_22533_amd import f3c
+    got, want = _gemm_case(torch, f3c.F3C_F32, epi, M, N, K, seed=M + N + K + epi)
+    assert max_rel(got, want) < 1e-5
+
+
+def _attn_case(torch, dt, heads, hd, q_lens, k_lens, seed, sample_queries=None):
+    from paper_2511_22533_amd import f3c
+    rng = np.random.default_rng(seed)
+    d = heads * hd
+    q_off = np.concatenate([[0], np.cumsum(q_lens)]).astype(int)
+    k_off = np.concatenate([[0], np.cumsum(k_lens)]).astype(int)
+    q = (1.5 * rng.standard_normal((q_off[-1], d))).astype(np.float32)
+    k = (1.5 * rng.standard_normal((k_off[-1], d))).astype(np.float32)
+    v = rng.standard_normal((k_off[-1], d)).astype(np.float32)
+    tdt = torch.bfloat16 if dt == f3c.F3C_BF16 else torch.float32
+    if dt == f3c.F3C_BF16:
+        q, k, v = bf16_round(q), bf16_round(k), bf16_round(v)
+    o = torch.zeros((max(q_off[-1], 1), d), dtype=tdt, device="cuda")
+    say("attention", dt, heads, hd, list(q_lens), list(k_lens))
+    f3c.op_attention(dt, heads, hd, q_off.tolist(), k_off.tolist(), to_dev(q, tdt), to_dev(k, tdt),
+                     to_dev(v, tdt), o)
+    torch.cuda.synchronize()
+    got = o.float().cpu().numpy()
+    worst = 0.0
+    for b in range(len(q_lens)):
+        if q_lens[b] == 0:
+            continue
+        rows = np.arange(q_off[b], q_off[b + 1])
+        if sample_queries and len(rows) > sample_queries:
+            rows = np.sort(rng.choice(rows, sample_queries, replace=False))
+        kk = k[k_off[b]:k_off[b + 1]].astype(np.float64)
+        vv = v[k_off[b]:k_off[b + 1]].astype(np.float64)
+        want = dit.attention(q[rows].astype(np.float64), kk, vv, heads)
+        worst = max(worst, max_rel(got[rows], want))
+    return worst
+
+
+@pytest.mark.parametrize("q_lens,k_lens", [([64], [64]), ([1], [1]), ([200], [200]), ([0, 37, 300], [0, 37, 300]),
+                                           ([820], [820]), ([615, 1536, 2458, 1003], [615, 1536, 2458, 1003])])
+def test_self_attention_bf16(torch, q_lens, k_lens):
+    from paper_2511_22533_amd import f3c
+    assert _attn_case(torch, f3c.F3C_BF16, 16, 64, q_lens, k_lens, seed=sum(q_lens)) < 2e-2
+
+
+def test_self_attention_bf16_full_size_sampled(torch):
+    from paper_2511_22533_amd import f3c
+    assert _attn_case(torch, f3c.F3C_BF16, 16, 64, [4096], [4096], seed=5, sample_queries=96) < 2e-2
+    assert _attn_case(torch, f3c.F3C_BF16, 16, 64, [9831], [9831], seed=6, sample_queries=64) < 2e-2
+
+
+@pytest.mark.parametrize("q_lens", [[820], [5, 1000, 0, 77]])
+def test_cross_attention_bf16(torch, q_lens):
+    from paper_2511_22533_amd import f3c
+    assert _attn_case(torch, f3c.F3C_BF16, 16, 64, q_lens, [1374] * len(q_lens), seed=len(q_lens)) < 2e-2
+
+
+@pytest.mark.parametrize("hd,heads", [(32, 4), (64, 2)])
+@pytest.mark.parametrize("q_lens,k_lens", [([512], [512]), ([3, 256, 130], [64, 64, 64]), ([100], [1])])
+def test_attention_f32(torch, hd, heads, q_lens, k_lens):
+    from paper_2511_22533_amd import f3c
+    assert _attn_case(torch, f3c.F3C_F32, heads, hd, q_lens, k_lens, seed=hd + len(q_lens)) < 1e-4
+
+
+def test_attention_bf16_hd32(torch):
+    from paper_2511_22533_amd import f3c
+    assert _attn_case(torch, f3c.F3C_BF16, 4, 32, [300, 64], [300, 64], seed=9) < 2e-2
+
+
+@pytest.mark.parametrize("dt_name,d", [("f32", 128), ("bf16", 1024), ("bf16", 2048)])
+def test_ln_mod(torch, dt_name, d):
+    from paper_2511_22533_amd import f3c
+    rng = np.random.default_rng(d)
+    rows = 333
+    h = (3 * rng.standard_normal((rows, d)) + 1).astype(np.float32)
+    shift = rng.standard_normal(d).astype(np.float32)
+    scale = rng.standard_normal(d).astype(np.float32)
+    dt = f3c.F3C_BF16 if dt_name == "bf16" else f3c.F3C_F32
+    tdt = torch.bfloat16 if dt_name == "bf16" else torch.float32
+    for mod in (True, False):
+        out = torch.empty((rows, d), dtype=tdt, device="cuda")
+        say("ln", dt_name, d, mod)
+        f3c.op_ln_mod(dt, to_dev(h), out, to_dev(shift) if mod else None, to_dev(scale) if mod else None)
+        torch.cuda.synchronize()
+        want = dit.layer_norm(h.astype(np.float64))
+        if mod:
+            want = want * (1 + scale) + shift
+        tol = 8e-3 if dt_name == "bf16" else 1e-5
+        assert max_rel(out.float().cpu().numpy(), want) < tol
+
+
+@pytest.mark.parametrize("cfg", [synth.TINY, synth.ModelConfig(grid=4, width=1024, depth=3, heads=16, cond_tokens=8,
+                                                              cond_width=64, dtype="bf16")])
+def test_modulation(torch, cfg):
+    from paper_2511_22533_amd import f3c
+    W = synth.make_weights(cfg, seed=2, scale=0.05)
+    m = f3c.Model(cfg).load(W)
+    om = dit.Model(cfg, W)
+    for t in (1.0, 0.73, 0.111, 0.0):
+        say("modulation", cfg.dtype, t)
+        got = m.modulation(t).cpu().numpy()
+        torch.cuda.synchronize()
+        tol = 1e-4 if cfg.dtype == "f32" else 5e-3
+        assert max_rel(got, om.modulation(t)) < tol

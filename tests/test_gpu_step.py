@@ -1,0 +1,216 @@
+"""GPU parity of whole cached steps and trajectories, through the C ABI.
+
+Per step (teacher-forced on the GPU's own pre-step state):
+* the selection equals the oracle's selection on the downloaded caches, bit
+  for bit (indices and position map);
+* the fresh velocities equal the oracle transformer on the same active set
+  within 1e-4 (f32 build) / 2e-2 (bf16) max-rel, per sample;
+* cached rows carry the stored velocity bit for bit, the Euler update and the
+  cache rotation are bit-exact given the merged velocity;
+Trajectories: final latents within 3e-2 relative L2 of the free-running oracle.
+Also: quota 0 equals the full step bit for bit, checkpoint export/import
+resumes bit-identically, and repeated runs are bit-identical.
+"""
+import numpy as np
+import pytest
+
+from helpers import Pair, depth_variant, max_rel, oracle_selection, rel_l2, say, to_dev
+from oracle import sampler, schedule
+from paper_2511_22533_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+F32 = np.float32
+
+
+def _gpu_step(torch, pair, x_dev, t, tn, n_cache):
+    before = pair.state.tensors()
+    torch.cuda.synchronize()
+    vc = before["v_cache"].cpu().numpy()
+    vp = before["v_prev"].cpu().numpy()
+    x_before = x_dev.cpu().numpy()
+    if any(n_cache):
+        pair.state.cached_step(x_dev, t, tn, n_cache)
+    else:
+        pair.state.full_step(x_dev, t, tn)
+    torch.cuda.synchronize()
+    after = pair.state.tensors()
+    return dict(vc=vc, vp=vp, x0=x_before, x1=x_dev.cpu().numpy(), idx=after["idx_active"].cpu().numpy(),
+                pos=after["pos"].cpu().numpy(), vact=after["v_act"].cpu().numpy(), off=after["act_off"],
+                vnew=after["v_cache"].cpu().numpy(), vold=after["v_prev"].cpu().numpy())
+
+
+def _check_step(pair, r, t, tn, n_cache, vel_tol, omega=0.7):
+    B, N = pair.B, pair.cfg.tokens
+    ref = oracle_selection(r["vc"], r["vp"], n_cache, omega)
+    dt = F32(t - tn)
+    worst = 0.0
+    for b in range(B):
+        active = ref[b][1]
+        lo, hi = r["off"][b], r["off"][b + 1]
+        assert hi - lo == N - n_cache[b]
+        if any(n_cache):
+            assert np.array_equal(r["idx"][lo:hi], active), f"selection sample {b}"
+            want_pos = np.full(N, -1)
+            want_pos[active] = lo + np.arange(hi - lo)
+            assert np.array_equal(r["pos"][b], want_pos)
+        # merged velocity: cached rows bit-identical, active rows from v_act
+        cached = np.setdiff1d(np.arange(N), active)
+        assert np.array_equal(r["vnew"][b][cached].view(np.uint32), r["vc"][b][cached].view(np.uint32))
+        assert np.array_equal(r["vnew"][b][active].view(np.uint32), r["vact"][lo:hi].view(np.uint32))
+        assert np.array_equal(r["vold"][b].view(np.uint32), r["vc"][b].view(np.uint32))
+        # Euler, bit-exact given the merged velocity
+        assert np.array_equal(r["x1"][b].view(np.uint32), (r["x0"][b] - dt * r["vnew"][b]).view(np.uint32))
+        # fresh velocities vs the oracle transformer on the same tokens
+        if hi > lo:
+            want = pair.oracle.forward(r["x0"][b][active], active, t, pair.cond[b])
+            err = max_rel(r["vact"][lo:hi], want)
+            worst = max(worst, err)
+            assert err < vel_tol, f"sample {b}: velocity max-rel {err}"
+    return worst
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    from paper_2511_22533_amd import f3c
+    f3c.lib()
+    return t
+
+
+def test_tiny_f32_trajectory(torch):
+    w = synth.WORKLOADS["tiny_f32"]
+    pair = Pair(w.model, w.batch)
+    times = schedule.time_grid(w.steps, w.shift)
+    quotas = synth.quota_schedule(w)
+    x = to_dev(pair.x_T)
+    for k in range(w.steps):
+        say("tiny_f32 step", k + 1, quotas[k].tolist())
+        r = _gpu_step(torch, pair, x, times[k], times[k + 1], quotas[k].tolist())
+        _check_step(pair, r, times[k], times[k + 1], quotas[k].tolist(), 1e-4)
+    final = x.cpu().numpy()
+    ref = sampler.sample(pair.x_T, pair.velocity(), times, quotas)
+    assert rel_l2(final, ref.x) < 3e-2
+    assert rel_l2(final, ref.x) < 1e-4
+
+
+def test_tiny_f32_amplified_sublayers(torch):
+    # larger weights: attention, cross-attention and MLP all move h by O(1)
+    cfg = synth.TINY
+    pair = Pair(cfg, 2, seed=5, scale=0.08)
+    x = to_dev(pair.x_T)
+    times = schedule.time_grid(6, 1.0)
+    for k, q in enumerate([[0, 0], [0, 0], [100, 300], [256, 0], [511, 1], [512, 200]]):
+        say("tiny amplified step", k + 1, q)
+        r = _gpu_step(torch, pair, x, times[k], times[k + 1], q)
+        _check_step(pair, r, times[k], times[k + 1], q, 1e-4)
+
+
+def test_quota_zero_equals_full_step_and_determinism(torch):
+    cfg = synth.TINY
+    a = Pair(cfg, 2, seed=1)
+    b = Pair(cfg, 2, seed=1)
+    xa, xb = to_dev(a.x_T), to_dev(b.x_T)
+    say("quota zero vs full")
+    a.state.full_step(xa, 1.0, 0.9)
+    b.state.cached_step(xb, 1.0, 0.9, [0, 0])
+    a.state.full_step(xa, 0.9, 0.8)
+    b.state.cached_step(xb, 0.9, 0.8, [0, 0])
+    a.state.cached_step(xa, 0.8, 0.7, [100, 200])
+    b.state.cached_step(xb, 0.8, 0.7, [100, 200])
+    torch.cuda.synchronize()
+    assert torch.equal(xa, xb)
+    assert np.array_equal(a.state.export(), b.state.export())
+
+
+def test_checkpoint_resume_bit_identical(torch):
+    cfg = synth.TINY
+    pair = Pair(cfg, 1, seed=3)
+    times = schedule.time_grid(8, 1.0)
+    q = [[0], [0], [0], [100], [200], [300], [400], [500]]
+    x = to_dev(pair.x_T)
+    say("checkpoint")
+    for k in range(4):
+        pair.state.cached_step(x, times[k], times[k + 1], q[k])
+    snap_x = x.clone()
+    snap = pair.state.export()
+    for k in range(4, 8):
+        pair.state.cached_step(x, times[k], times[k + 1], q[k])
+    torch.cuda.synchronize()
+    first = x.clone()
+    pair.state.import_(snap)
+    x.copy_(snap_x)
+    for k in range(4, 8):
+        pair.state.cached_step(x, times[k], times[k + 1], q[k])
+    torch.cuda.synchronize()
+    assert torch.equal(first, x)
+
+
+def test_trellis16_cached_step_full_depth(torch):
+    """Full-size model (24 blocks, width 1024, 4096 tokens), cached step at 80% quota."""
+    cfg = synth.TRELLIS16
+    pair = Pair(cfg, 1)
+    rng = np.random.default_rng(7)
+    x = to_dev(pair.x_T)
+    vc = (0.5 * rng.standard_normal((1, cfg.tokens, 8))).astype(F32)
+    vp = (vc + 0.05 * rng.standard_normal(vc.shape)).astype(F32)
+    pair.state.import_(np.concatenate([vc.ravel(), vp.ravel()]))
+    t = schedule.time_grid(25, 3.0)
+    say("trellis16 cached step k=25")
+    r = _gpu_step(torch, pair, x, t[24], t[25], [3276])
+    err = _check_step(pair, r, t[24], t[25], [3276], 2e-2)
+    say("trellis16 cached max-rel", err)
+
+
+def test_trellis16_full_step_two_blocks(torch):
+    cfg = depth_variant(synth.TRELLIS16, 2)
+    pair = Pair(cfg, 1)
+    x = to_dev(pair.x_T)
+    say("trellis16 depth-2 full step")
+    r = _gpu_step(torch, pair, x, 1.0, 0.98630136986301364, [0])
+    _check_step(pair, r, 1.0, 0.98630136986301364, [0], 2e-2)
+
+
+def test_trellis16_batch4_ragged_cached_step(torch):
+    cfg = depth_variant(synth.TRELLIS16, 2)
+    pair = Pair(cfg, 4)
+    rng = np.random.default_rng(8)
+    x = to_dev(pair.x_T)
+    vc = (0.5 * rng.standard_normal((4, cfg.tokens, 8))).astype(F32)
+    vp = (vc + 0.05 * rng.standard_normal(vc.shape)).astype(F32)
+    pair.state.import_(np.concatenate([vc.ravel(), vp.ravel()]))
+    q = synth.quota_schedule(synth.WORKLOADS["trellis16_cached_b4"])[-1].tolist()
+    say("trellis16 b4 ragged", q)
+    r = _gpu_step(torch, pair, x, 0.3, 0.25, q)
+    _check_step(pair, r, 0.3, 0.25, q, 2e-2)
+
+
+def test_trellis32_cached_step_one_block(torch):
+    cfg = depth_variant(synth.TRELLIS32, 1)
+    pair = Pair(cfg, 1)
+    rng = np.random.default_rng(9)
+    x = to_dev(pair.x_T)
+    vc = (0.5 * rng.standard_normal((1, cfg.tokens, 8))).astype(F32)
+    vp = (vc + 0.05 * rng.standard_normal(vc.shape)).astype(F32)
+    pair.state.import_(np.concatenate([vc.ravel(), vp.ravel()]))
+    say("trellis32 cached 70%")
+    r = _gpu_step(torch, pair, x, 0.5, 0.45, [22937])
+    _check_step(pair, r, 0.5, 0.45, [22937], 2e-2)
+
+
+def test_trellis16_trajectory_one_block(torch):
+    """25 shifted steps with the seeded logistic quota: final latent within 3e-2 rel L2."""
+    w = synth.WORKLOADS["trellis16_cached"]
+    cfg = depth_variant(w.model, 1)
+    pair = Pair(cfg, 1)
+    times = schedule.time_grid(w.steps, w.shift)
+    quotas = synth.quota_schedule(w)
+    x = to_dev(pair.x_T)
+    for k in range(w.steps):
+        say("trellis16 trajectory step", k + 1)
+        pair.state.cached_step(x, times[k], times[k + 1], quotas[k].tolist())
+    torch.cuda.synchronize()
+    ref = sampler.sample(pair.x_T, pair.velocity(), times, quotas)
+    err = rel_l2(x.cpu().numpy(), ref.x)
+    say("trajectory rel L2", err)
+    assert err < 3e-2
