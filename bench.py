@@ -1,0 +1,224 @@
+"""Throughput of the cached sparse-structure flow-DiT sampler on one MI355X.
+
+Workload (default): the 24-block, width-1024 TRELLIS-shaped sparse-structure
+transformer on a 16^3 latent grid (4096 tokens, 8 channels), 16 heads of 64,
+cross-attention to 1374 condition tokens of width 1024, bf16, batch 1, 25
+shifted Euler steps: 5 full steps, then a seeded logistic cache quota that
+reaches 80% cached tokens at step 25. Weights, noise and condition tokens are
+seeded synthetic data (no trained weights or image features exist here).
+
+A "step" is one denoising step of that schedule: stability scoring and top-k
+selection, gather + embedding, timestep modulation, 24 blocks on the active
+tokens, output projection and the merge/Euler/cache update. K timed steps walk
+through the schedule and wrap around; every trajectory start re-zeroes the
+caches, reloads x_T and recomputes the condition keys/values inside the timed
+region.
+
+Prints one JSON line. ``value`` is denoising steps per second; the line also
+carries active tokens/s, the whole-step MFMA fraction (FLOPs model of the
+supplement over wall time), the roofline entry of the dominant kernel (HIP
+events on the launch stream around each of its launches in the timed region)
+and the CPU oracle baseline (a bounded sample timed on this host).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3       # MI355X fp32 matrix/vector
+PEAK_HBM_GBS = 8000.0
+DENSE_CLASSES = ["gemm_qkv", "attn_self", "gemm_o", "gemm_q", "attn_cross", "gemm_co", "gemm_fc1", "gemm_fc2"]
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=25)
+    ap.add_argument("--workload", default="trellis16_cached")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-depth", type=int, default=8, help="oracle blocks timed (0 = full depth)")
+    return ap.parse_args()
+
+
+def cpu_baseline(w, W, cond, x_T, quotas, times, depth):
+    """Time the CPU oracle on a bounded sample: one full step and one cached step
+    (the schedule's last quota), at `depth` blocks, scaled to the whole model and
+    interpolated over the schedule by the FLOPs model."""
+    from oracle import dit, flops, sampler, ssc
+    from paper_2511_22533_amd import synth
+    cfg = w.model
+    depth = depth or cfg.depth
+    sub = synth.ModelConfig(grid=cfg.grid, width=cfg.width, depth=depth, heads=cfg.heads,
+                            cond_tokens=cfg.cond_tokens, cond_width=cfg.cond_width, dtype=cfg.dtype,
+                            mlp_ratio=cfg.mlp_ratio)
+    model = dit.Model(sub, W)
+    vel = sampler.model_velocity(model, cond)
+    st = sampler.State.start(x_T)
+    rng = np.random.default_rng(0)
+    st.v_cache[:] = rng.standard_normal(st.v_cache.shape).astype(np.float32)
+    st.v_prev[:] = rng.standard_normal(st.v_prev.shape).astype(np.float32)
+    n_last = int(quotas[-1][0])
+    t0 = time.perf_counter()
+    sampler.step(st, vel, times[0], times[1], [0] * w.batch)
+    t_full = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    sampler.step(st, vel, times[-2], times[-1], quotas[-1])
+    t_cached = time.perf_counter() - t0
+    scale = cfg.depth / depth
+    N = cfg.tokens
+    f_full = flops.forward_flops(cfg, N, 1)
+    f_last = flops.forward_flops(cfg, N - n_last, 1)
+    total = 0.0
+    tokens = 0
+    for q in quotas:
+        n = N - int(q[0])
+        f = flops.forward_flops(cfg, n, 1)
+        frac = (f - f_last) / (f_full - f_last) if f_full > f_last else 1.0
+        total += scale * (t_cached + (t_full - t_cached) * frac)
+        tokens += n * w.batch
+    steps = len(quotas)
+    threads = len(os.sched_getaffinity(0))
+    return {
+        "value": steps / total,
+        "unit": "steps/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"float64 NumPy oracle, {depth} of {cfg.depth} blocks: one full step ({N} tokens, "
+                   f"{t_full:.2f} s) and one cached step ({N - n_last} active, {t_cached:.2f} s), scaled by "
+                   f"{scale:g} to all blocks and interpolated over the {steps}-step schedule with the FLOPs model"),
+        "active_tokens_per_s": tokens / total,
+        "seconds_measured": t_full + t_cached,
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import torch
+    from paper_2511_22533_amd import f3c, synth
+    from paper_2511_22533_amd.f3c import PROF_CLASSES
+
+    w = synth.WORKLOADS[args.workload]
+    cfg = w.model
+    torch.cuda.set_device(0)
+    print(f"[bench] workload {w.name}: {w.description}", file=sys.stderr, flush=True)
+    W = synth.make_weights(cfg)
+    cond = synth.make_cond(cfg, w.batch)
+    x_T = synth.make_noise(cfg, w.batch)
+    quotas = synth.quota_schedule(w)
+    times = f3c.time_grid(w.steps, w.shift)
+    model = f3c.Model(cfg).load(W)
+    state = f3c.State(model, w.batch)
+    x = torch.empty((w.batch, cfg.tokens, cfg.in_ch), dtype=torch.float32, device="cuda")
+    x_T_dev = torch.from_numpy(x_T).cuda()
+    cond_dev = torch.from_numpy(cond).cuda()
+    T = w.steps
+
+    def run_step(i):
+        k = i % T
+        if k == 0:
+            state.reset()
+            x.copy_(x_T_dev)
+            state.set_cond(cond_dev)
+        q = quotas[k].tolist()
+        if any(q):
+            state.cached_step(x, float(times[k]), float(times[k + 1]), q)
+        else:
+            state.full_step(x, float(times[k]), float(times[k + 1]))
+        return sum(cfg.tokens - c for c in q)
+
+    # warmup (untimed)
+    for i in range(args.warmup):
+        run_step(i)
+    torch.cuda.synchronize()
+    print(f"[bench] warmup {args.warmup} steps done", file=sys.stderr, flush=True)
+
+    # calibration pass (untimed): which dense kernel class takes the most time
+    state.profile(True)
+    state.profile_reset()
+    for i in range(T):
+        run_step(i)
+    torch.cuda.synchronize()
+    calib = state.profile_read()
+    state.profile(False)
+    state.profile_reset()
+    dominant = max(DENSE_CLASSES, key=lambda c: calib[c]["ms"])
+    print(f"[bench] per-class ms over one trajectory: "
+          + ", ".join(f"{c}={calib[c]['ms']:.2f}" for c in PROF_CLASSES if calib[c]["launches"]),
+          file=sys.stderr, flush=True)
+
+    # timed region: K steps from a trajectory start, events only around the dominant class
+    state.profile([dominant])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    active = 0
+    flop_total = 0.0
+    for i in range(args.steps):
+        n_act = run_step(i)
+        active += n_act
+        flop_total += sum(f3c.forward_flops(cfg, cfg.tokens - int(c), 1) for c in quotas[i % T])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    prof = state.profile_read()[dominant]
+    state.profile(False)
+    print(f"[bench] timed {args.steps} steps in {elapsed * 1e3:.1f} ms", file=sys.stderr, flush=True)
+
+    peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
+    achieved = prof["flops"] / (prof["ms"] * 1e-3) / 1e12 if prof["ms"] > 0 else 0.0
+    roofline = {
+        "bound": "mfma",
+        "kernel": dominant,
+        "achieved": round(achieved, 2),
+        "peak": peak,
+        "unit": "TFLOP/s",
+        "frac": round(achieved / peak, 4),
+        "traffic": None,
+        "launches": prof["launches"],
+        "avg_launch_us": round(prof["ms"] * 1e3 / max(prof["launches"], 1), 2),
+        "flops_per_launch": prof["flops"] / max(prof["launches"], 1),
+    }
+    step_tflops = flop_total / elapsed / 1e12
+    out = {
+        "metric": "denoising steps/s (cached flow-DiT sampler)",
+        "value": round(args.steps / elapsed, 3),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(elapsed * 1e3 / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded weights, noise and condition tokens)",
+        "config": {"workload": w.name, "grid": cfg.grid, "tokens": cfg.tokens, "width": cfg.width,
+                   "depth": cfg.depth, "heads": cfg.heads, "cond_tokens": cfg.cond_tokens, "batch": w.batch,
+                   "steps_per_trajectory": T, "quota": w.schedule, "parallelism": "single GPU"},
+        "active_tokens_per_s": round(active / elapsed, 1),
+        "step_model_tflops": round(step_tflops, 2),
+        "step_mfma_frac": round(step_tflops / peak, 4),
+        "roofline": roofline,
+    }
+    if not args.no_cpu:
+        print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(w, W, cond, x_T, quotas, times, args.cpu_depth)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -153,8 +153,9 @@ int f3c_state_record_scores(f3c_state* s, int32_t on);
 int f3c_state_export(const f3c_state* s, float* host, size_t n_floats, f3c_stream stream);
 int f3c_state_import(f3c_state* s, const float* host, size_t n_floats, f3c_stream stream);
 
-/* Per-kernel-class timing with HIP events recorded around each launch on the
- * launch stream while enabled. read synchronises the recorded events and
+/* Per-kernel-class timing with HIP events recorded around each launch of the
+ * classes selected by `mask` (bit c = class c; 0 disables) on the launch
+ * stream. read synchronises the recorded events and
  * returns launches, total milliseconds and total algorithmic FLOPs (dense
  * contractions: 2*M*N*K; attention: the QK^T and PV terms of the FLOPs model)
  * and algorithmic bytes (memory-bound kernels). */
@@ -174,7 +175,7 @@ int f3c_state_import(f3c_state* s, const float* host, size_t n_floats, f3c_strea
 #define F3C_PROF_EULER 13
 #define F3C_PROF_COND 14
 #define F3C_PROF_CLASSES 15
-int f3c_profile_enable(f3c_state* s, int32_t on);
+int f3c_profile_enable(f3c_state* s, uint32_t mask);
 int f3c_profile_read(f3c_state* s, int32_t cls, int64_t* launches, double* ms, double* flops, double* bytes);
 int f3c_profile_reset(f3c_state* s);
 

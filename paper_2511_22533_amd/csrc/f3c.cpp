@@ -84,7 +84,8 @@ struct f3c_state {
   float *h, *vact, *mod, *temb, *score;
   void *u, *qkv, *att, *qc, *hid, *cond_t, *kv;
   int32_t *idx, *pos;
-  bool cond_set = false, record_scores = false, profiling = false;
+  bool cond_set = false, record_scores = false;
+  uint32_t prof_mask = 0;
   float omega = 0.7f;
   Segs last_act{};
   Prof prof[F3C_PROF_CLASSES];
@@ -111,7 +112,7 @@ struct Scope {
   hipStream_t st;
   hipEvent_t e1 = nullptr;
   Scope(f3c_state* s_, int cls_, hipStream_t st_, double flops, double bytes) : s(s_), cls(cls_), st(st_) {
-    if (!s->profiling) return;
+    if (!(s->prof_mask >> cls & 1u)) return;
     hipEvent_t e0 = take_event(s);
     e1 = take_event(s);
     if (!e0 || !e1) { e1 = nullptr; return; }
@@ -224,7 +225,7 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
       }
       {
         Scope sc(s, F3C_PROF_GEMM_QKV, st, 2.0 * rows * 3 * d * d, 0);
-        HIP_TRY(launch_gemm(dt, EPI_STORE, rows, 3 * d, d, s->u, d, m->w(p + "qkv_w"), d, m->b(p + "qkv_b"),
+        HIP_TRY(launch_gemm(SITE_QKV, dt, EPI_STORE, rows, 3 * d, d, s->u, d, m->w(p + "qkv_w"), d, m->b(p + "qkv_b"),
                             nullptr, s->qkv, 3 * d, nullptr, 0, st));
       }
       {
@@ -232,12 +233,12 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
         for (int b = 0; b < B; ++b) fl += 4.0 * (double)(act.off[b + 1] - act.off[b]) * (act.off[b + 1] - act.off[b]) * d;
         Scope sc(s, F3C_PROF_ATTN_SELF, st, fl, 0);
         const char* q = static_cast<const char*>(s->qkv);
-        HIP_TRY(launch_attention(dt, m->cfg.heads, m->hd, act, act, q, 3 * d, q + d * es, 3 * d, q + 2 * d * es,
+        HIP_TRY(launch_attention(SITE_SELF, dt, m->cfg.heads, m->hd, act, act, q, 3 * d, q + d * es, 3 * d, q + 2 * d * es,
                                  3 * d, s->att, d, st));
       }
       {
         Scope sc(s, F3C_PROF_GEMM_O, st, 2.0 * rows * d * d, 0);
-        HIP_TRY(launch_gemm(dt, EPI_RESID, rows, d, d, s->att, d, m->w(p + "o_w"), d, m->b(p + "o_b"), md + 2 * d,
+        HIP_TRY(launch_gemm(SITE_O, dt, EPI_RESID, rows, d, d, s->att, d, m->w(p + "o_w"), d, m->b(p + "o_b"), md + 2 * d,
                             nullptr, 0, s->h, d, st));
       }
       {
@@ -246,18 +247,18 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
       }
       {
         Scope sc(s, F3C_PROF_GEMM_Q, st, 2.0 * rows * d * d, 0);
-        HIP_TRY(launch_gemm(dt, EPI_STORE, rows, d, d, s->u, d, m->w(p + "q_w"), d, m->b(p + "q_b"), nullptr,
+        HIP_TRY(launch_gemm(SITE_Q, dt, EPI_STORE, rows, d, d, s->u, d, m->w(p + "q_w"), d, m->b(p + "q_b"), nullptr,
                             s->qc, d, nullptr, 0, st));
       }
       {
         Scope sc(s, F3C_PROF_ATTN_CROSS, st, 4.0 * rows * m->Nc * d, 0);
         const char* kv = static_cast<const char*>(s->kv) + (size_t)l * 2 * d * es;
-        HIP_TRY(launch_attention(dt, m->cfg.heads, m->hd, act, cond_segs, s->qc, d, kv, 2 * L * d, kv + d * es,
+        HIP_TRY(launch_attention(SITE_CROSS, dt, m->cfg.heads, m->hd, act, cond_segs, s->qc, d, kv, 2 * L * d, kv + d * es,
                                  2 * L * d, s->att, d, st));
       }
       {
         Scope sc(s, F3C_PROF_GEMM_CO, st, 2.0 * rows * d * d, 0);
-        HIP_TRY(launch_gemm(dt, EPI_RESID, rows, d, d, s->att, d, m->w(p + "co_w"), d, m->b(p + "co_b"), nullptr,
+        HIP_TRY(launch_gemm(SITE_CO, dt, EPI_RESID, rows, d, d, s->att, d, m->w(p + "co_w"), d, m->b(p + "co_b"), nullptr,
                             nullptr, 0, s->h, d, st));
       }
       {
@@ -266,12 +267,12 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
       }
       {
         Scope sc(s, F3C_PROF_GEMM_FC1, st, 2.0 * rows * dm * d, 0);
-        HIP_TRY(launch_gemm(dt, EPI_GELU, rows, dm, d, s->u, d, m->w(p + "fc1_w"), d, m->b(p + "fc1_b"), nullptr,
+        HIP_TRY(launch_gemm(SITE_FC1, dt, EPI_GELU, rows, dm, d, s->u, d, m->w(p + "fc1_w"), d, m->b(p + "fc1_b"), nullptr,
                             s->hid, dm, nullptr, 0, st));
       }
       {
         Scope sc(s, F3C_PROF_GEMM_FC2, st, 2.0 * rows * d * dm, 0);
-        HIP_TRY(launch_gemm(dt, EPI_RESID, rows, d, dm, s->hid, dm, m->w(p + "fc2_w"), dm, m->b(p + "fc2_b"),
+        HIP_TRY(launch_gemm(SITE_FC2, dt, EPI_RESID, rows, d, dm, s->hid, dm, m->w(p + "fc2_w"), dm, m->b(p + "fc2_b"),
                             md + 5 * d, nullptr, 0, s->h, d, st));
       }
     }
@@ -523,7 +524,7 @@ int f3c_set_cond(f3c_state* s, const float* cond_dev, f3c_stream stream) {
   const int rows = s->B * m->Nc, n = 2 * m->L * m->d;
   Scope sc(s, F3C_PROF_COND, st, 2.0 * rows * n * m->dc, 0);
   HIP_TRY(launch_convert(m->cfg.dtype, cond_dev, s->cond_t, (int64_t)rows * m->dc, st));
-  HIP_TRY(launch_gemm(m->cfg.dtype, EPI_STORE, rows, n, m->dc, s->cond_t, m->dc, m->wdev + m->kv_w, m->dc,
+  HIP_TRY(launch_gemm(SITE_COND, m->cfg.dtype, EPI_STORE, rows, n, m->dc, s->cond_t, m->dc, m->wdev + m->kv_w, m->dc,
                       (const float*)(m->wdev + m->kv_b), nullptr, s->kv, n, nullptr, 0, st));
   s->cond_set = true;
   return F3C_OK;
@@ -596,9 +597,9 @@ int f3c_state_import(f3c_state* s, const float* host, size_t n_floats, f3c_strea
   return F3C_OK;
 }
 
-int f3c_profile_enable(f3c_state* s, int32_t on) {
+int f3c_profile_enable(f3c_state* s, uint32_t mask) {
   if (!s) return fail(F3C_EINVAL, "state is NULL");
-  s->profiling = on != 0;
+  s->prof_mask = mask & ((1u << F3C_PROF_CLASSES) - 1u);
   return F3C_OK;
 }
 
@@ -667,7 +668,7 @@ int f3c_op_gemm(int32_t dtype, int32_t epilogue, int32_t M, int32_t N, int32_t K
   if (lda < K || ldw < K || (lda * es) % 16 || (ldw * es) % 16) return fail(F3C_EINVAL, "bad leading dims");
   if (!A || !W || !bias) return fail(F3C_EINVAL, "NULL operand");
   if (epilogue == 2 ? (!resid || ldr < N) : (!out || ldo < N)) return fail(F3C_EINVAL, "bad output");
-  HIP_TRY(launch_gemm(dtype, epilogue, M, N, K, A, lda, W, ldw, bias, gate, out, ldo, resid, ldr,
+  HIP_TRY(launch_gemm(SITE_OP, dtype, epilogue, M, N, K, A, lda, W, ldw, bias, gate, out, ldo, resid, ldr,
                       (hipStream_t)stream));
   return F3C_OK;
 }
@@ -695,7 +696,7 @@ int f3c_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int32_t bat
   for (int b = 0; b < batch; ++b)
     if (qs.off[b + 1] > qs.off[b] && ks.off[b + 1] == ks.off[b])
       return fail(F3C_EINVAL, "sample %d has queries but no keys", b);
-  HIP_TRY(launch_attention(dtype, heads, head_dim, qs, ks, q, ldq, k, ldk, v, ldv, o, ldo, (hipStream_t)stream));
+  HIP_TRY(launch_attention(SITE_OP, dtype, heads, head_dim, qs, ks, q, ldq, k, ldk, v, ldv, o, ldo, (hipStream_t)stream));
   return F3C_OK;
 }
 

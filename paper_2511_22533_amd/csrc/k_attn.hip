@@ -31,7 +31,7 @@ struct AttnArgs {
   float scale_log2;              // log2(e) / sqrt(hd)
 };
 
-template <typename T, int HD>
+template <typename T, int HD, int SITE>
 __global__ __launch_bounds__(256) void k_attn(AttnArgs p) {
   constexpr int ES = sizeof(T);
   constexpr int E = Mfma<T>::E;
@@ -185,10 +185,20 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs p) {
     for (int e = 0; e < 16; ++e) orow[t * 32 + 8 * (e >> 2) + 4 * g + (e & 3)] = from_f32<T>(oacc[t][e] * inv);
 }
 
+template <int SITE>
+hipError_t launch_a(int dt, int hd, dim3 grid, const AttnArgs& a, hipStream_t s) {
+  if (dt == DT_BF16 && hd == 64) hipLaunchKernelGGL((k_attn<bf16, 64, SITE>), grid, dim3(256), 0, s, a);
+  else if (dt == DT_BF16 && hd == 32) hipLaunchKernelGGL((k_attn<bf16, 32, SITE>), grid, dim3(256), 0, s, a);
+  else if (dt == DT_F32 && hd == 64) hipLaunchKernelGGL((k_attn<float, 64, SITE>), grid, dim3(256), 0, s, a);
+  else if (dt == DT_F32 && hd == 32) hipLaunchKernelGGL((k_attn<float, 32, SITE>), grid, dim3(256), 0, s, a);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
 }  // namespace
 
-hipError_t launch_attention(int dt, int heads, int hd, const Segs& qs, const Segs& ks, const void* q, int ldq,
-                            const void* k, int ldk, const void* v, int ldv, void* o, int ldo, hipStream_t s) {
+hipError_t launch_attention(int site, int dt, int heads, int hd, const Segs& qs, const Segs& ks, const void* q,
+                            int ldq, const void* k, int ldk, const void* v, int ldv, void* o, int ldo, hipStream_t s) {
   AttnArgs a;
   a.qs = qs;
   a.ks = ks;
@@ -206,12 +216,9 @@ hipError_t launch_attention(int dt, int heads, int hd, const Segs& qs, const Seg
   a.ldo = ldo;
   a.scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
   dim3 grid(tiles, heads);
-  if (dt == DT_BF16 && hd == 64) hipLaunchKernelGGL((k_attn<bf16, 64>), grid, dim3(256), 0, s, a);
-  else if (dt == DT_BF16 && hd == 32) hipLaunchKernelGGL((k_attn<bf16, 32>), grid, dim3(256), 0, s, a);
-  else if (dt == DT_F32 && hd == 64) hipLaunchKernelGGL((k_attn<float, 64>), grid, dim3(256), 0, s, a);
-  else if (dt == DT_F32 && hd == 32) hipLaunchKernelGGL((k_attn<float, 32>), grid, dim3(256), 0, s, a);
-  else return hipErrorInvalidValue;
-  return hipGetLastError();
+  if (site == SITE_SELF) return launch_a<SITE_SELF>(dt, hd, grid, a, s);
+  if (site == SITE_CROSS) return launch_a<SITE_CROSS>(dt, hd, grid, a, s);
+  return launch_a<SITE_OP>(dt, hd, grid, a, s);
 }
 
 }  // namespace f3c

@@ -37,7 +37,7 @@ struct GemmArgs {
   int ldr;
 };
 
-template <typename T, int BM, int BN, int EPI>
+template <typename T, int BM, int BN, int EPI, int SITE>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs p) {
   constexpr int TM = BM / 64, TN = BN / 64;                 // 32x32 tiles per wave
   constexpr int CA = BM * 8 / 256, CB = BN * 8 / 256;       // 16-byte chunks per thread
@@ -156,35 +156,42 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs p) {
     }
 }
 
-template <typename T, int EPI>
+template <typename T, int EPI, int SITE>
 hipError_t launch_t(const GemmArgs& a, hipStream_t s) {
   constexpr int BM = 128, BN = 128;
   dim3 grid(a.N / BN, (a.M + BM - 1) / BM);
-  hipLaunchKernelGGL((k_gemm<T, BM, BN, EPI>), grid, dim3(256), 0, s, a);
+  hipLaunchKernelGGL((k_gemm<T, BM, BN, EPI, SITE>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_site(int site, int epi, const GemmArgs& a, hipStream_t s) {
+  switch (site) {
+    case SITE_QKV: return launch_t<T, EPI_STORE, SITE_QKV>(a, s);
+    case SITE_Q: return launch_t<T, EPI_STORE, SITE_Q>(a, s);
+    case SITE_COND: return launch_t<T, EPI_STORE, SITE_COND>(a, s);
+    case SITE_O: return launch_t<T, EPI_RESID, SITE_O>(a, s);
+    case SITE_CO: return launch_t<T, EPI_RESID, SITE_CO>(a, s);
+    case SITE_FC2: return launch_t<T, EPI_RESID, SITE_FC2>(a, s);
+    case SITE_FC1: return launch_t<T, EPI_GELU, SITE_FC1>(a, s);
+    default: break;
+  }
+  switch (epi) {
+    case EPI_STORE: return launch_t<T, EPI_STORE, SITE_OP>(a, s);
+    case EPI_GELU: return launch_t<T, EPI_GELU, SITE_OP>(a, s);
+    case EPI_RESID: return launch_t<T, EPI_RESID, SITE_OP>(a, s);
+  }
+  return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-hipError_t launch_gemm(int dt, int epi, int M, int N, int K, const void* A, int lda, const void* W, int ldw,
-                       const float* bias, const float* gate, void* out, int ldo, float* resid, int ldr,
+hipError_t launch_gemm(int site, int dt, int epi, int M, int N, int K, const void* A, int lda, const void* W,
+                       int ldw, const float* bias, const float* gate, void* out, int ldo, float* resid, int ldr,
                        hipStream_t s) {
   if (M == 0) return hipSuccess;
   GemmArgs a{M, N, K, (const char*)A, lda, (const char*)W, ldw, bias, gate, out, ldo, resid, ldr};
-  if (dt == DT_BF16) {
-    switch (epi) {
-      case EPI_STORE: return launch_t<bf16, EPI_STORE>(a, s);
-      case EPI_GELU: return launch_t<bf16, EPI_GELU>(a, s);
-      case EPI_RESID: return launch_t<bf16, EPI_RESID>(a, s);
-    }
-  } else {
-    switch (epi) {
-      case EPI_STORE: return launch_t<float, EPI_STORE>(a, s);
-      case EPI_GELU: return launch_t<float, EPI_GELU>(a, s);
-      case EPI_RESID: return launch_t<float, EPI_RESID>(a, s);
-    }
-  }
-  return hipErrorInvalidValue;
+  return dt == DT_BF16 ? launch_site<bf16>(site, epi, a, s) : launch_site<float>(site, epi, a, s);
 }
 
 }  // namespace f3c

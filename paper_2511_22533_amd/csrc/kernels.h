@@ -19,6 +19,10 @@ struct Segs {
 enum Dtype { DT_F32 = 0, DT_BF16 = 1 };
 enum Epilogue { EPI_STORE = 0, EPI_GELU = 1, EPI_RESID = 2 };
 
+// Call sites of the dense kernels. Each site is its own template instance, so a
+// kernel trace attributes time to the projection / attention it belongs to.
+enum Site { SITE_OP = 0, SITE_QKV, SITE_O, SITE_Q, SITE_CO, SITE_FC1, SITE_FC2, SITE_COND, SITE_SELF, SITE_CROSS };
+
 // Stability score + lowest-score selection, one workgroup per sample.
 // v_cache, v_prev: f32 [B][N][8]. n_cache: per-sample cached counts (by value).
 // act: active-row offsets (by value). Writes idx_active[act.off[b] + r] (ascending
@@ -59,14 +63,14 @@ hipError_t launch_convert(int dt, const float* src, void* dst, int64_t n, hipStr
 // bias f32 [N]. EPI_STORE / EPI_GELU write out[M][ldo] in the model dtype;
 // EPI_RESID does resid[m][n] += (gate ? gate[n] : 1) * value in f32.
 // Requires N % 128 == 0 and K % (128 / sizeof(element)) == 0.
-hipError_t launch_gemm(int dt, int epi, int M, int N, int K, const void* A, int lda, const void* W, int ldw,
-                       const float* bias, const float* gate, void* out, int ldo, float* resid, int ldr,
+hipError_t launch_gemm(int site, int dt, int epi, int M, int N, int K, const void* A, int lda, const void* W,
+                       int ldw, const float* bias, const float* gate, void* out, int ldo, float* resid, int ldr,
                        hipStream_t s);
 
 // Varlen multi-head softmax attention. Queries of sample b are rows
 // [qs.off[b], qs.off[b+1]) of q; its keys/values are rows [ks.off[b], ks.off[b+1])
 // of k and v. Head h uses columns [h*hd, (h+1)*hd). Output rows match queries.
-hipError_t launch_attention(int dt, int heads, int hd, const Segs& qs, const Segs& ks, const void* q, int ldq,
-                            const void* k, int ldk, const void* v, int ldv, void* o, int ldo, hipStream_t s);
+hipError_t launch_attention(int site, int dt, int heads, int hd, const Segs& qs, const Segs& ks, const void* q,
+                            int ldq, const void* k, int ldk, const void* v, int ldv, void* o, int ldo, hipStream_t s);
 
 }  // namespace f3c

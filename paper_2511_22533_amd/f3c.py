@@ -65,7 +65,7 @@ _SIGS = {
     "f3c_state_record_scores": (c_int, [c_p, c_int]),
     "f3c_state_export": (c_int, [c_p, P_f, c_sz, c_p]),
     "f3c_state_import": (c_int, [c_p, P_f, c_sz, c_p]),
-    "f3c_profile_enable": (c_int, [c_p, c_int]),
+    "f3c_profile_enable": (c_int, [c_p, ctypes.c_uint32]),
     "f3c_profile_read": (c_int, [c_p, c_int, ctypes.POINTER(c_i64), P_d, P_d, P_d]),
     "f3c_profile_reset": (c_int, [c_p]),
     "f3c_op_select": (c_int, [c_int, c_int, c_p, c_p, c_f, P_i32, c_p, c_p, c_p, c_p]),
@@ -294,8 +294,17 @@ class State:
         host = np.ascontiguousarray(host, dtype=np.float32)
         check(lib().f3c_state_import(self.h, host.ctypes.data_as(P_f), host.size, _stream(stream)))
 
-    def profile(self, on: bool):
-        check(lib().f3c_profile_enable(self.h, int(on)))
+    def profile(self, classes=None):
+        """Record HIP events around launches of the named kernel classes (all if True, none if falsy)."""
+        if classes is True:
+            mask = (1 << len(PROF_CLASSES)) - 1
+        elif not classes:
+            mask = 0
+        else:
+            mask = 0
+            for c in classes:
+                mask |= 1 << PROF_CLASSES.index(c)
+        check(lib().f3c_profile_enable(self.h, mask))
 
     def profile_reset(self):
         check(lib().f3c_profile_reset(self.h))
