@@ -3,13 +3,20 @@
 // attention runs on the active subset only) and for cross-attention from the
 // active tokens to the image-condition tokens.
 //
-// Online softmax over key/value tiles of 64 staged in LDS (V is stored
+// Online softmax over key/value tiles of 64 staged in LDS (V stored
 // transposed). Each wavefront owns 32 queries and computes S^T = K Q^T, so a
 // lane holds one query's scores for 16 of every 32 keys: the running max and
 // sum are per-lane values combined with a single cross-half exchange
 // (lane l with l ^ 32). The same accumulator layout feeds O^T = V^T P^T as the
 // B operand without any data movement; the K-slot order of P (keys
 // 8*(e/4) + 4*(l/32) + e%4) is matched when the V^T fragment is read.
+//
+// Pipelining: the next K/V tile is fetched into registers while the current
+// one is consumed, then written to the other LDS buffer (one barrier per
+// tile). Only the last, ragged tile is masked. The running max is updated
+// lazily: the accumulators are rescaled only when some query's max grows by
+// more than 2^8 (in base-2 units), which keeps every unnormalised probability
+// below 2^8 and the result unchanged up to rounding.
 #include "common.h"
 #include "kernels.h"
 
@@ -17,8 +24,8 @@ namespace f3c {
 
 namespace {
 
-constexpr int kBQ = 128;    // queries per workgroup (4 waves x 32)
-constexpr int kBKV = 64;    // keys per LDS tile
+constexpr int kBKV = 64;             // keys per LDS tile
+constexpr float kRescaleLog2 = 8.0f;
 
 struct AttnArgs {
   Segs qs, ks;
@@ -31,8 +38,10 @@ struct AttnArgs {
   float scale_log2;              // log2(e) / sqrt(hd)
 };
 
-template <typename T, int HD, int SITE>
-__global__ __launch_bounds__(256) void k_attn(AttnArgs p) {
+template <typename T, int HD, int NW, int SITE>
+__global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
+  constexpr int NT = 64 * NW;
+  constexpr int BQ = 32 * NW;
   constexpr int ES = sizeof(T);
   constexpr int E = Mfma<T>::E;
   constexpr int KRS = HD * ES + 16;          // K tile row stride (bytes)
@@ -41,9 +50,13 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs p) {
   constexpr int PER16 = 16 / ES;
   constexpr int MMA_PER_READ = PER16 / E;
   constexpr int HT = HD / 32;                // 32-row output tiles over the head dim
-  constexpr int CH = kBKV * HD * ES / 16;    // 16-byte chunks per K (or V) tile
-  __shared__ __attribute__((aligned(16))) char Ks[kBKV * KRS];
-  __shared__ __attribute__((aligned(16))) char Vt[HD * VRS];
+  constexpr int CPR = HD * ES / 16;          // 16-byte chunks per key row
+  constexpr int KITEMS = kBKV * CPR;        // K chunks per tile
+  constexpr int VITEMS = kBKV / 2 * CPR;    // V (key pair, chunk) items per tile
+  constexpr int KCH = (KITEMS + NT - 1) / NT;
+  constexpr int VPR = (VITEMS + NT - 1) / NT;
+  constexpr int KBUF = kBKV * KRS, VBUF = HD * VRS;
+  __shared__ __attribute__((aligned(16))) char lds[2 * (KBUF + VBUF)];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 5, r32 = lane & 31;
@@ -52,7 +65,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs p) {
   const int qt = blockIdx.x - p.tile_off[b];
   const int q_begin = p.qs.off[b], nq = p.qs.off[b + 1] - q_begin;
   const int k_begin = p.ks.off[b], nk = p.ks.off[b + 1] - k_begin;
-  const int qi = qt * kBQ + wave * 32 + r32;          // query of this lane (within the sample)
+  const int qi = qt * BQ + wave * 32 + r32;            // query of this lane (within the sample)
   const bool q_ok = qi < nq;
 
   // Q^T as the B operand: lane reads 16 bytes of its query row per 32-byte slice.
@@ -64,32 +77,73 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs p) {
       qf[s] = q_ok ? *reinterpret_cast<const u32x4*>(qrow + s * 32 + g * 16) : u32x4{0, 0, 0, 0};
   }
 
+  // Tile staging: K row-major, V transposed (pairs of keys per 32/64-bit write).
+  // Keys past the end are read from the last key (always valid) and masked.
+  u32x4 rk[KCH], rv[VPR][2];
+  auto fetch = [&](int kv0) {
+#pragma unroll
+    for (int q = 0; q < KCH; ++q) {
+      const int ch = tid + NT * q, row = ch / CPR, col = ch % CPR;
+      if (KITEMS % NT != 0 && ch >= KITEMS) break;
+      const int key = min(kv0 + row, nk - 1);
+      rk[q] = *reinterpret_cast<const u32x4*>(p.k + ((size_t)(k_begin + key) * p.ldk + head * HD) * ES + col * 16);
+    }
+#pragma unroll
+    for (int q = 0; q < VPR; ++q) {
+      const int it = tid + NT * q, pr = it / CPR, col = it % CPR;
+      if (VITEMS % NT != 0 && it >= VITEMS) break;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int key = min(kv0 + 2 * pr + h, nk - 1);
+        rv[q][h] = *reinterpret_cast<const u32x4*>(p.v + ((size_t)(k_begin + key) * p.ldv + head * HD) * ES + col * 16);
+      }
+    }
+  };
+  auto stage = [&](int buf) {
+    char* Ks = lds + buf * (KBUF + VBUF);
+    char* Vt = Ks + KBUF;
+#pragma unroll
+    for (int q = 0; q < KCH; ++q) {
+      const int ch = tid + NT * q, row = ch / CPR, col = ch % CPR;
+      if (KITEMS % NT != 0 && ch >= KITEMS) break;
+      *reinterpret_cast<u32x4*>(Ks + row * KRS + col * 16) = rk[q];
+    }
+#pragma unroll
+    for (int q = 0; q < VPR; ++q) {
+      const int it = tid + NT * q, pr = it / CPR, col = it % CPR;
+      if (VITEMS % NT != 0 && it >= VITEMS) break;
+      const T* v0 = reinterpret_cast<const T*>(&rv[q][0]);
+      const T* v1 = reinterpret_cast<const T*>(&rv[q][1]);
+#pragma unroll
+      for (int e = 0; e < PER16; ++e) {
+        char* dst = Vt + (col * PER16 + e) * VRS + 2 * pr * ES;
+        if constexpr (ES == 2) {
+          const uint32_t lo = __builtin_bit_cast(uint16_t, v0[e]), hi = __builtin_bit_cast(uint16_t, v1[e]);
+          *reinterpret_cast<uint32_t*>(dst) = lo | (hi << 16);
+        } else {
+          *reinterpret_cast<float2*>(dst) = make_float2(v0[e], v1[e]);
+        }
+      }
+    }
+  };
+
   f32x16 oacc[HT];
 #pragma unroll
   for (int t = 0; t < HT; ++t)
 #pragma unroll
     for (int e = 0; e < 16; ++e) oacc[t][e] = 0.0f;
-  float m_run = -INFINITY, l_run = 0.0f;
+  float m_run = -INFINITY, l_run = 0.0f;       // running max (raw logits), unnormalised sum
   const float c = p.scale_log2;
+  const int ntiles = (nk + kBKV - 1) / kBKV;
 
-  for (int kv0 = 0; kv0 < nk; kv0 += kBKV) {
-    // Stage K (row-major) and V (transposed) for keys kv0 .. kv0+63.
-#pragma unroll
-    for (int q = 0; q < CH / 256; ++q) {
-      const int ch = tid + 256 * q;
-      const int row = ch / (HD * ES / 16), col = ch % (HD * ES / 16);
-      const bool ok = kv0 + row < nk;
-      const size_t key = (size_t)(k_begin + kv0 + row);
-      u32x4 kk = ok ? *reinterpret_cast<const u32x4*>(p.k + (key * p.ldk + head * HD) * ES + col * 16)
-                    : u32x4{0, 0, 0, 0};
-      u32x4 vv = ok ? *reinterpret_cast<const u32x4*>(p.v + (key * p.ldv + head * HD) * ES + col * 16)
-                    : u32x4{0, 0, 0, 0};
-      *reinterpret_cast<u32x4*>(Ks + row * KRS + col * 16) = kk;
-      const T* ve = reinterpret_cast<const T*>(&vv);
-#pragma unroll
-      for (int e = 0; e < PER16; ++e) *reinterpret_cast<T*>(Vt + (col * PER16 + e) * VRS + row * ES) = ve[e];
-    }
-    __syncthreads();
+  fetch(0);
+  stage(0);
+  __syncthreads();
+  for (int t = 0; t < ntiles; ++t) {
+    const int kv0 = t * kBKV;
+    if (t + 1 < ntiles) fetch(kv0 + kBKV);
+    const char* Ks = lds + (t & 1) * (KBUF + VBUF);
+    const char* Vt = Ks + KBUF;
 
     // S^T tiles: rows = keys kv0 + 32*kt + ..., cols = this wave's 32 queries.
     f32x16 sacc[2];
@@ -115,26 +169,32 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs p) {
       }
     }
 
-    // Online softmax (base 2). Key of element e: kv0 + 32*kt + 8*(e/4) + 4*g + e%4.
-    float mx = -INFINITY;
+    // Key of element e: kv0 + 32*kt + 8*(e/4) + 4*g + e%4. Mask the ragged tail.
+    if (kv0 + kBKV > nk) {
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+      for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int key = kv0 + kt * 32 + 8 * (e >> 2) + 4 * g + (e & 3);
-        if (key >= nk) sacc[kt][e] = -INFINITY;
-        mx = fmaxf(mx, sacc[kt][e]);
-      }
+        for (int e = 0; e < 16; ++e)
+          if (kv0 + kt * 32 + 8 * (e >> 2) + 4 * g + (e & 3) >= nk) sacc[kt][e] = -INFINITY;
+    }
+    float mx = fmaxf(sacc[0][0], sacc[0][1]);
+#pragma unroll
+    for (int e = 2; e < 16; e += 2) mx = fmaxf(mx, fmaxf(sacc[0][e], sacc[0][e + 1]));
+#pragma unroll
+    for (int e = 0; e < 16; e += 2) mx = fmaxf(mx, fmaxf(sacc[1][e], sacc[1][e + 1]));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c);
-    const float mc = m_new * c;
-    m_run = m_new;
-    l_run *= alpha;
+    // Lazy rescale: move the reference max only when it grows by more than 2^8.
+    if (__builtin_amdgcn_ballot_w64((mx - m_run) * c > kRescaleLog2) != 0) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c);
+      m_run = m_new;
+      l_run *= alpha;
 #pragma unroll
-    for (int t = 0; t < HT; ++t)
+      for (int u = 0; u < HT; ++u)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) oacc[t][e] *= alpha;
+        for (int e = 0; e < 16; ++e) oacc[u][e] *= alpha;
+    }
+    const float mc = m_run * c;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
@@ -157,8 +217,8 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs p) {
           pf = sacc[kt][u];
         }
 #pragma unroll
-        for (int t = 0; t < HT; ++t) {
-          const char* vrow = Vt + (t * 32 + r32) * VRS;
+        for (int h = 0; h < HT; ++h) {
+          const char* vrow = Vt + (h * 32 + r32) * VRS;
           typename Mfma<T>::frag vf;
           if constexpr (ES == 2) {
             const int key0 = kt * 32 + 16 * u + 4 * g;
@@ -169,9 +229,10 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs p) {
             const int key = kt * 32 + 8 * (u >> 2) + 4 * g + (u & 3);
             vf = *reinterpret_cast<const float*>(vrow + key * ES);
           }
-          oacc[t] = Mfma<T>::mma(vf, pf, oacc[t]);
+          oacc[h] = Mfma<T>::mma(vf, pf, oacc[h]);
         }
       }
+    if (t + 1 < ntiles) stage((t + 1) & 1);
     __syncthreads();
   }
 
@@ -180,19 +241,49 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs p) {
   const float inv = 1.0f / l_tot;
   T* orow = reinterpret_cast<T*>(p.o + ((size_t)(q_begin + qi) * p.ldo + head * HD) * ES);
 #pragma unroll
-  for (int t = 0; t < HT; ++t)
+  for (int h = 0; h < HT; ++h)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) orow[t * 32 + 8 * (e >> 2) + 4 * g + (e & 3)] = from_f32<T>(oacc[t][e] * inv);
+    for (int q4 = 0; q4 < 4; ++q4) {
+      float v[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = oacc[h][4 * q4 + e] * inv;
+      T* dst = orow + h * 32 + 8 * q4 + 4 * g;
+      if constexpr (ES == 2) {
+        bf16x4 o4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o4[e] = (bf16)v[e];
+        *reinterpret_cast<bf16x4*>(dst) = o4;
+      } else {
+        *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+      }
+    }
 }
 
-template <int SITE>
-hipError_t launch_a(int dt, int hd, dim3 grid, const AttnArgs& a, hipStream_t s) {
-  if (dt == DT_BF16 && hd == 64) hipLaunchKernelGGL((k_attn<bf16, 64, SITE>), grid, dim3(256), 0, s, a);
-  else if (dt == DT_BF16 && hd == 32) hipLaunchKernelGGL((k_attn<bf16, 32, SITE>), grid, dim3(256), 0, s, a);
-  else if (dt == DT_F32 && hd == 64) hipLaunchKernelGGL((k_attn<float, 64, SITE>), grid, dim3(256), 0, s, a);
-  else if (dt == DT_F32 && hd == 32) hipLaunchKernelGGL((k_attn<float, 32, SITE>), grid, dim3(256), 0, s, a);
+template <int NW, int SITE>
+hipError_t launch_a(int dt, int hd, const AttnArgs& a0, int heads, hipStream_t s) {
+  AttnArgs a = a0;
+  constexpr int BQ = 32 * NW;
+  a.tile_off[0] = 0;
+  for (int b = 0; b < a.qs.B; ++b) a.tile_off[b + 1] = a.tile_off[b] + (a.qs.off[b + 1] - a.qs.off[b] + BQ - 1) / BQ;
+  const int tiles = a.tile_off[a.qs.B];
+  if (tiles == 0) return hipSuccess;
+  dim3 grid(tiles, heads), block(64 * NW);
+  if (dt == DT_BF16 && hd == 64) hipLaunchKernelGGL((k_attn<bf16, 64, NW, SITE>), grid, block, 0, s, a);
+  else if (dt == DT_BF16 && hd == 32) hipLaunchKernelGGL((k_attn<bf16, 32, NW, SITE>), grid, block, 0, s, a);
+  else if (dt == DT_F32 && hd == 64) hipLaunchKernelGGL((k_attn<float, 64, NW, SITE>), grid, block, 0, s, a);
+  else if (dt == DT_F32 && hd == 32) hipLaunchKernelGGL((k_attn<float, 32, NW, SITE>), grid, block, 0, s, a);
   else return hipErrorInvalidValue;
   return hipGetLastError();
+}
+
+// 4 waves (128 queries) per workgroup when that still gives about two
+// workgroups per CU, else 2 waves (64 queries).
+template <int SITE>
+hipError_t launch_site(int dt, int hd, const AttnArgs& a, int heads, hipStream_t s) {
+  long t128 = 0;
+  for (int b = 0; b < a.qs.B; ++b) t128 += (a.qs.off[b + 1] - a.qs.off[b] + 127) / 128;
+  if (t128 * heads >= 480) return launch_a<4, SITE>(dt, hd, a, heads, s);
+  return launch_a<2, SITE>(dt, hd, a, heads, s);
 }
 
 }  // namespace
@@ -202,10 +293,6 @@ hipError_t launch_attention(int site, int dt, int heads, int hd, const Segs& qs,
   AttnArgs a;
   a.qs = qs;
   a.ks = ks;
-  a.tile_off[0] = 0;
-  for (int b = 0; b < qs.B; ++b) a.tile_off[b + 1] = a.tile_off[b] + (qs.off[b + 1] - qs.off[b] + kBQ - 1) / kBQ;
-  const int tiles = a.tile_off[qs.B];
-  if (tiles == 0) return hipSuccess;
   a.q = (const char*)q;
   a.k = (const char*)k;
   a.v = (const char*)v;
@@ -215,10 +302,9 @@ hipError_t launch_attention(int site, int dt, int heads, int hd, const Segs& qs,
   a.ldv = ldv;
   a.ldo = ldo;
   a.scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
-  dim3 grid(tiles, heads);
-  if (site == SITE_SELF) return launch_a<SITE_SELF>(dt, hd, grid, a, s);
-  if (site == SITE_CROSS) return launch_a<SITE_CROSS>(dt, hd, grid, a, s);
-  return launch_a<SITE_OP>(dt, hd, grid, a, s);
+  if (site == SITE_SELF) return launch_site<SITE_SELF>(dt, hd, a, heads, s);
+  if (site == SITE_CROSS) return launch_site<SITE_CROSS>(dt, hd, a, heads, s);
+  return launch_site<SITE_OP>(dt, hd, a, heads, s);
 }
 
 }  // namespace f3c

@@ -5,14 +5,20 @@
 // GELU (tanh form, MLP fc1), or a gated residual update in f32
 // (h += gate * (.), attention output projections and MLP fc2).
 //
-// Workgroup tile BM x BN, K staged 128 bytes at a time through padded LDS rows
-// (144-byte stride: the 16-byte fragment reads of 8 consecutive lanes land on
-// disjoint banks). 4 wavefronts in a 2 x 2 arrangement; each owns a
-// (BM/2) x (BN/2) sub-tile of 32x32 MFMA accumulators. The next K tile is
-// prefetched into registers while the current one is consumed from LDS.
-// A lane reads 16 contiguous bytes of one row at K-group offset l/32; the same
-// K mapping is used for A and W, so any assignment of K elements to the
-// instruction's K slots gives the same dot products.
+// Workgroup tile BM x BN with 4 wavefronts in a 2 x 2 arrangement, each owning
+// a (BM/2) x (BN/2) block of 32x32 MFMA accumulators. K is staged 128 bytes at
+// a time through padded LDS rows (144-byte stride: the 16-byte fragment reads
+// of 16 consecutive lanes cover all 64 banks once). The next K tile is fetched
+// into registers while the current one is consumed, and written to the second
+// LDS buffer, so one barrier per K tile suffices.
+//
+// The weight fragment is the MFMA's A operand and the activation fragment its
+// B operand, i.e. each instruction produces a 32 x 32 tile of C^T: a lane then
+// holds one activation row and four consecutive output columns per
+// accumulator group, so the epilogue moves 8-byte (bf16) / 16-byte (f32)
+// vectors. A lane reads 16 contiguous bytes of one row at K-group offset l/32
+// for both operands; any common assignment of K elements to the instruction's
+// K slots yields the same dot products.
 #include "common.h"
 #include "kernels.h"
 
@@ -37,51 +43,76 @@ struct GemmArgs {
   int ldr;
 };
 
-template <typename T, int BM, int BN, int EPI, int SITE>
-__global__ __launch_bounds__(256) void k_gemm(GemmArgs p) {
-  constexpr int TM = BM / 64, TN = BN / 64;                 // 32x32 tiles per wave
-  constexpr int CA = BM * 8 / 256, CB = BN * 8 / 256;       // 16-byte chunks per thread
+template <typename T>
+__device__ __forceinline__ void store4(T* dst, const float (&v)[4]);
+template <>
+__device__ __forceinline__ void store4<float>(float* dst, const float (&v)[4]) {
+  *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+}
+template <>
+__device__ __forceinline__ void store4<bf16>(bf16* dst, const float (&v)[4]) {
+  bf16x4 o;
+  o[0] = (bf16)v[0];
+  o[1] = (bf16)v[1];
+  o[2] = (bf16)v[2];
+  o[3] = (bf16)v[3];
+  *reinterpret_cast<bf16x4*>(dst) = o;
+}
+
+template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, int EPI, int SITE>
+__global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs p) {
+  constexpr int NT = 64 * WGM * WGN;                        // threads
+  constexpr int WTM = BM / WGM, WTN = BN / WGN;             // wave tile
+  constexpr int TM = WTM / 32, TN = WTN / 32;               // 32x32 tiles per wave
+  constexpr int CA = BM * 8 / NT, CB = BN * 8 / NT;         // 16-byte chunks per thread
   constexpr int ES = sizeof(T);
   constexpr int PER16 = 16 / ES;                            // elements per 16 bytes
   constexpr int MMA_PER_READ = PER16 / Mfma<T>::E;          // instructions per fragment read
-  __shared__ __attribute__((aligned(16))) char As[BM * kRS];
-  __shared__ __attribute__((aligned(16))) char Bs[BN * kRS];
+  constexpr int ABUF = BM * kRS, BBUF = BN * kRS;
+  static_assert(CA >= 1 && CB >= 1 && TM >= 1 && TN >= 1, "tile too small for the workgroup");
+  __shared__ __attribute__((aligned(16))) char lds[STAGES * (ABUF + BBUF)];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WGN, wn = wave % WGN;
   const int g = lane >> 5, r32 = lane & 31;
   const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
   const size_t lda_b = (size_t)p.lda * ES, ldw_b = (size_t)p.ldw * ES;
+  // Split-K: slice z of gridDim.z covers K tiles [z*KT, (z+1)*KT).
+  const int KT = (p.K * ES) / kBKB / (int)gridDim.z;
+  const size_t k_base = (size_t)blockIdx.z * KT * kBKB;
+
+  // Rows past M are loaded from row M-1 (always valid) and never stored.
+  const char* a_row[CA];
+  const char* w_row[CB];
+  int chunk_a[CA], chunk_b[CB];
+#pragma unroll
+  for (int q = 0; q < CA; ++q) {
+    const int c = tid + NT * q, row = c >> 3;
+    a_row[q] = p.A + (size_t)min(m0 + row, p.M - 1) * lda_b + k_base + (c & 7) * 16;
+    chunk_a[q] = row * kRS + (c & 7) * 16;
+  }
+#pragma unroll
+  for (int q = 0; q < CB; ++q) {
+    const int c = tid + NT * q, row = c >> 3;
+    w_row[q] = p.W + (size_t)(n0 + row) * ldw_b + k_base + (c & 7) * 16;
+    chunk_b[q] = row * kRS + (c & 7) * 16;
+  }
 
   u32x4 ra[CA], rb[CB];
   auto load_tile = [&](int kt) {
     const size_t kb = (size_t)kt * kBKB;
 #pragma unroll
-    for (int q = 0; q < CA; ++q) {
-      const int c = tid + 256 * q, row = c >> 3, col = c & 7;
-      const int m = m0 + row;
-      if (m < p.M)
-        ra[q] = *reinterpret_cast<const u32x4*>(p.A + (size_t)m * lda_b + kb + col * 16);
-      else
-        ra[q] = u32x4{0, 0, 0, 0};
-    }
+    for (int q = 0; q < CA; ++q) ra[q] = *reinterpret_cast<const u32x4*>(a_row[q] + kb);
 #pragma unroll
-    for (int q = 0; q < CB; ++q) {
-      const int c = tid + 256 * q, row = c >> 3, col = c & 7;
-      rb[q] = *reinterpret_cast<const u32x4*>(p.W + (size_t)(n0 + row) * ldw_b + kb + col * 16);
-    }
+    for (int q = 0; q < CB; ++q) rb[q] = *reinterpret_cast<const u32x4*>(w_row[q] + kb);
   };
-  auto store_tile = [&]() {
+  auto store_tile = [&](int buf) {
+    char* As = lds + buf * (ABUF + BBUF);
+    char* Bs = As + ABUF;
 #pragma unroll
-    for (int q = 0; q < CA; ++q) {
-      const int c = tid + 256 * q, row = c >> 3, col = c & 7;
-      *reinterpret_cast<u32x4*>(As + row * kRS + col * 16) = ra[q];
-    }
+    for (int q = 0; q < CA; ++q) *reinterpret_cast<u32x4*>(As + chunk_a[q]) = ra[q];
 #pragma unroll
-    for (int q = 0; q < CB; ++q) {
-      const int c = tid + 256 * q, row = c >> 3, col = c & 7;
-      *reinterpret_cast<u32x4*>(Bs + row * kRS + col * 16) = rb[q];
-    }
+    for (int q = 0; q < CB; ++q) *reinterpret_cast<u32x4*>(Bs + chunk_b[q]) = rb[q];
   };
 
   f32x16 acc[TM][TN];
@@ -92,94 +123,194 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs p) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
-  const int KT = (p.K * ES) / kBKB;
-  load_tile(0);
-  store_tile();
-  __syncthreads();
-  for (int kt = 0; kt < KT; ++kt) {
-    if (kt + 1 < KT) load_tile(kt + 1);
+  auto compute = [&](int buf) {
+    const char* As = lds + buf * (ABUF + BBUF);
+    const char* Bs = As + ABUF;
 #pragma unroll
     for (int ks = 0; ks < kBKB / 32; ++ks) {
       u32x4 fa[TM], fb[TN];
 #pragma unroll
       for (int i = 0; i < TM; ++i)
-        fa[i] = *reinterpret_cast<const u32x4*>(As + (wm * (BM / 2) + i * 32 + r32) * kRS + ks * 32 + g * 16);
+        fa[i] = *reinterpret_cast<const u32x4*>(As + (wm * WTM + i * 32 + r32) * kRS + ks * 32 + g * 16);
 #pragma unroll
       for (int j = 0; j < TN; ++j)
-        fb[j] = *reinterpret_cast<const u32x4*>(Bs + (wn * (BN / 2) + j * 32 + r32) * kRS + ks * 32 + g * 16);
+        fb[j] = *reinterpret_cast<const u32x4*>(Bs + (wn * WTN + j * 32 + r32) * kRS + ks * 32 + g * 16);
 #pragma unroll
       for (int u = 0; u < MMA_PER_READ; ++u)
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
           for (int j = 0; j < TN; ++j) {
-            typename Mfma<T>::frag a, b;
+            typename Mfma<T>::frag a, w;
             if constexpr (sizeof(T) == 2) {
               a = __builtin_bit_cast(bf16x8, fa[i]);
-              b = __builtin_bit_cast(bf16x8, fb[j]);
+              w = __builtin_bit_cast(bf16x8, fb[j]);
             } else {
               a = __builtin_bit_cast(f32x4, fa[i])[u];
-              b = __builtin_bit_cast(f32x4, fb[j])[u];
+              w = __builtin_bit_cast(f32x4, fb[j])[u];
             }
-            acc[i][j] = Mfma<T>::mma(a, b, acc[i][j]);
+            acc[i][j] = Mfma<T>::mma(w, a, acc[i][j]);   // C^T tile: rows = output columns
           }
     }
-    __syncthreads();
-    if (kt + 1 < KT) {
-      store_tile();
+  };
+
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
+  for (int kt = 0; kt < KT; ++kt) {
+    if (kt + 1 < KT) load_tile(kt + 1);
+    if constexpr (STAGES == 2) {
+      compute(kt & 1);
+      if (kt + 1 < KT) store_tile((kt + 1) & 1);
       __syncthreads();
+    } else {
+      compute(0);
+      __syncthreads();
+      if (kt + 1 < KT) {
+        store_tile(0);
+        __syncthreads();
+      }
     }
   }
 
-  // Epilogue: lane holds column r32 and rows 8*(e/4) + 4*g + e%4 of each tile.
+  // Epilogue. Tile (i, j), group q: activation row m0 + wm*BM/2 + 32 i + r32,
+  // output columns n0 + wn*BN/2 + 32 j + 8 q + 4 g + (0..3).
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+  for (int i = 0; i < TM; ++i) {
+    const int row = m0 + wm * WTM + i * 32 + r32;
+    if (row >= p.M) continue;
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int col = n0 + wn * (BN / 2) + j * 32 + r32;
-      const float bcol = p.bias[col];
-      const float gcol = (EPI == EPI_RESID && p.gate) ? p.gate[col] : 1.0f;
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int row = m0 + wm * (BM / 2) + i * 32 + 8 * (e >> 2) + 4 * g + (e & 3);
-        if (row >= p.M) continue;
-        const float v = acc[i][j][e] + bcol;
+      for (int q = 0; q < 4; ++q) {
+        const int col = n0 + wn * WTN + j * 32 + 8 * q + 4 * g;
+        if constexpr (EPI == EPI_PARTIAL) {
+          float* part = p.resid + ((size_t)blockIdx.z * p.M + row) * p.N + col;
+          *reinterpret_cast<float4*>(part) =
+              make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+          continue;
+        }
+        const float4 bv = *reinterpret_cast<const float4*>(p.bias + col);
+        float v[4] = {acc[i][j][4 * q] + bv.x, acc[i][j][4 * q + 1] + bv.y, acc[i][j][4 * q + 2] + bv.z,
+                      acc[i][j][4 * q + 3] + bv.w};
         if constexpr (EPI == EPI_RESID) {
-          float* r = p.resid + (size_t)row * p.ldr + col;
-          *r = *r + gcol * v;
-        } else if constexpr (EPI == EPI_GELU) {
-          reinterpret_cast<T*>(p.out)[(size_t)row * p.ldo + col] = from_f32<T>(gelu_tanh(v));
+          float4 gv = make_float4(1.0f, 1.0f, 1.0f, 1.0f);
+          if (p.gate) gv = *reinterpret_cast<const float4*>(p.gate + col);
+          float4* r = reinterpret_cast<float4*>(p.resid + (size_t)row * p.ldr + col);
+          float4 h = *r;
+          h.x += gv.x * v[0];
+          h.y += gv.y * v[1];
+          h.z += gv.z * v[2];
+          h.w += gv.w * v[3];
+          *r = h;
         } else {
-          reinterpret_cast<T*>(p.out)[(size_t)row * p.ldo + col] = from_f32<T>(v);
+          if constexpr (EPI == EPI_GELU) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = gelu_tanh(v[e]);
+          }
+          store4<T>(reinterpret_cast<T*>(p.out) + (size_t)row * p.ldo + col, v);
         }
       }
-    }
+  }
 }
 
+// Split-K reduction: value = sum over slices in slice order (deterministic) +
+// bias, then the site's epilogue. One thread per 4 consecutive outputs.
 template <typename T, int EPI, int SITE>
-hipError_t launch_t(const GemmArgs& a, hipStream_t s) {
-  constexpr int BM = 128, BN = 128;
+__global__ __launch_bounds__(256) void k_splitk_reduce(GemmArgs p, const float* __restrict__ part, int splits) {
+  const int64_t i4 = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t total4 = (int64_t)p.M * p.N / 4;
+  if (i4 >= total4) return;
+  const int row = (int)(i4 * 4 / p.N), col = (int)(i4 * 4 % p.N);
+  float4 acc = *reinterpret_cast<const float4*>(part + (size_t)row * p.N + col);
+  for (int z = 1; z < splits; ++z) {
+    const float4 v = *reinterpret_cast<const float4*>(part + ((size_t)z * p.M + row) * p.N + col);
+    acc.x += v.x;
+    acc.y += v.y;
+    acc.z += v.z;
+    acc.w += v.w;
+  }
+  const float4 bv = *reinterpret_cast<const float4*>(p.bias + col);
+  float v[4] = {acc.x + bv.x, acc.y + bv.y, acc.z + bv.z, acc.w + bv.w};
+  if constexpr (EPI == EPI_RESID) {
+    float4 gv = make_float4(1.0f, 1.0f, 1.0f, 1.0f);
+    if (p.gate) gv = *reinterpret_cast<const float4*>(p.gate + col);
+    float4* r = reinterpret_cast<float4*>(p.resid + (size_t)row * p.ldr + col);
+    float4 h = *r;
+    h.x += gv.x * v[0];
+    h.y += gv.y * v[1];
+    h.z += gv.z * v[2];
+    h.w += gv.w * v[3];
+    *r = h;
+  } else {
+    if constexpr (EPI == EPI_GELU) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = gelu_tanh(v[e]);
+    }
+    store4<T>(reinterpret_cast<T*>(p.out) + (size_t)row * p.ldo + col, v);
+  }
+}
+
+template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, int EPI, int SITE>
+hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
   dim3 grid(a.N / BN, (a.M + BM - 1) / BM);
-  hipLaunchKernelGGL((k_gemm<T, BM, BN, EPI, SITE>), grid, dim3(256), 0, s, a);
+  hipLaunchKernelGGL((k_gemm<T, BM, BN, WGM, WGN, STAGES, EPI, SITE>), grid, dim3(64 * WGM * WGN), 0, s, a);
   return hipGetLastError();
 }
 
+// 64 x 64 tiles over `splits` K slices into f32 partials, then the reduction.
+template <typename T, int EPI, int SITE>
+hipError_t launch_splitk(const GemmArgs& a, int splits, float* ws, hipStream_t s) {
+  GemmArgs pa = a;
+  pa.resid = ws;
+  dim3 grid(a.N / 64, (a.M + 63) / 64, splits);
+  hipLaunchKernelGGL((k_gemm<T, 64, 64, 2, 2, 2, EPI_PARTIAL, SITE>), grid, dim3(256), 0, s, pa);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t total4 = (int64_t)a.M * a.N / 4;
+  hipLaunchKernelGGL((k_splitk_reduce<T, EPI, SITE>), dim3((unsigned)((total4 + 255) / 256)), dim3(256), 0, s, a, ws,
+                     splits);
+  return hipGetLastError();
+}
+
+// Tile choice (measured on MI355X at M = 820 ... 4096, N = 1024 ... 4096):
+// 128 x 128 with 8 waves while that gives >= 2 workgroups per CU, else 64 x 128
+// single-buffered, else 64 x 64; long-K shapes with few 64 x 64 tiles are split
+// along K when a workspace is available.
+template <typename T, int EPI, int SITE>
+hipError_t launch_t(const GemmArgs& a, float* ws, size_t ws_bytes, hipStream_t s) {
+  auto tiles = [&](int bm, int bn) { return (long)((a.M + bm - 1) / bm) * (a.N / bn); };
+  if constexpr (sizeof(T) == 2) {
+    if (tiles(128, 128) >= 512) return launch_cfg<T, 128, 128, 2, 4, 2, EPI, SITE>(a, s);
+    if (tiles(64, 128) >= 512) return launch_cfg<T, 64, 128, 2, 2, 1, EPI, SITE>(a, s);
+    const long t64 = tiles(64, 64);
+    const int kt = a.K * (int)sizeof(T) / kBKB;
+    int splits = 1;
+    while (splits < 4 && t64 * splits < 512 && kt % (2 * splits) == 0 && kt / (2 * splits) >= 8) splits *= 2;
+    if (splits > 1 && ws && (size_t)splits * a.M * a.N * sizeof(float) <= ws_bytes)
+      return launch_splitk<T, EPI, SITE>(a, splits, ws, s);
+    return launch_cfg<T, 64, 64, 2, 2, 2, EPI, SITE>(a, s);
+  } else {
+    return launch_cfg<T, 64, 128, 2, 2, 2, EPI, SITE>(a, s);
+  }
+}
+
 template <typename T>
-hipError_t launch_site(int site, int epi, const GemmArgs& a, hipStream_t s) {
+hipError_t launch_site(int site, int epi, const GemmArgs& a, float* ws, size_t wsb, hipStream_t s) {
   switch (site) {
-    case SITE_QKV: return launch_t<T, EPI_STORE, SITE_QKV>(a, s);
-    case SITE_Q: return launch_t<T, EPI_STORE, SITE_Q>(a, s);
-    case SITE_COND: return launch_t<T, EPI_STORE, SITE_COND>(a, s);
-    case SITE_O: return launch_t<T, EPI_RESID, SITE_O>(a, s);
-    case SITE_CO: return launch_t<T, EPI_RESID, SITE_CO>(a, s);
-    case SITE_FC2: return launch_t<T, EPI_RESID, SITE_FC2>(a, s);
-    case SITE_FC1: return launch_t<T, EPI_GELU, SITE_FC1>(a, s);
+    case SITE_QKV: return launch_t<T, EPI_STORE, SITE_QKV>(a, ws, wsb, s);
+    case SITE_Q: return launch_t<T, EPI_STORE, SITE_Q>(a, ws, wsb, s);
+    case SITE_COND: return launch_t<T, EPI_STORE, SITE_COND>(a, ws, wsb, s);
+    case SITE_O: return launch_t<T, EPI_RESID, SITE_O>(a, ws, wsb, s);
+    case SITE_CO: return launch_t<T, EPI_RESID, SITE_CO>(a, ws, wsb, s);
+    case SITE_FC2: return launch_t<T, EPI_RESID, SITE_FC2>(a, ws, wsb, s);
+    case SITE_FC1: return launch_t<T, EPI_GELU, SITE_FC1>(a, ws, wsb, s);
     default: break;
   }
   switch (epi) {
-    case EPI_STORE: return launch_t<T, EPI_STORE, SITE_OP>(a, s);
-    case EPI_GELU: return launch_t<T, EPI_GELU, SITE_OP>(a, s);
-    case EPI_RESID: return launch_t<T, EPI_RESID, SITE_OP>(a, s);
+    case EPI_STORE: return launch_t<T, EPI_STORE, SITE_OP>(a, ws, wsb, s);
+    case EPI_GELU: return launch_t<T, EPI_GELU, SITE_OP>(a, ws, wsb, s);
+    case EPI_RESID: return launch_t<T, EPI_RESID, SITE_OP>(a, ws, wsb, s);
   }
   return hipErrorInvalidValue;
 }
@@ -188,10 +319,11 @@ hipError_t launch_site(int site, int epi, const GemmArgs& a, hipStream_t s) {
 
 hipError_t launch_gemm(int site, int dt, int epi, int M, int N, int K, const void* A, int lda, const void* W,
                        int ldw, const float* bias, const float* gate, void* out, int ldo, float* resid, int ldr,
-                       hipStream_t s) {
+                       float* ws, size_t ws_bytes, hipStream_t s) {
   if (M == 0) return hipSuccess;
   GemmArgs a{M, N, K, (const char*)A, lda, (const char*)W, ldw, bias, gate, out, ldo, resid, ldr};
-  return dt == DT_BF16 ? launch_site<bf16>(site, epi, a, s) : launch_site<float>(site, epi, a, s);
+  return dt == DT_BF16 ? launch_site<bf16>(site, epi, a, ws, ws_bytes, s)
+                       : launch_site<float>(site, epi, a, ws, ws_bytes, s);
 }
 
 }  // namespace f3c
