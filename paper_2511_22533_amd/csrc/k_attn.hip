@@ -150,8 +150,6 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) sacc[kt][e] = 0.0f;
-#pragma unroll
       for (int s = 0; s < NKS; ++s) {
         const u32x4 kf = *reinterpret_cast<const u32x4*>(Ks + (kt * 32 + r32) * KRS + s * 32 + g * 16);
 #pragma unroll
@@ -164,7 +162,8 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
             a = __builtin_bit_cast(f32x4, kf)[u];
             bq = __builtin_bit_cast(f32x4, qf[s])[u];
           }
-          sacc[kt] = Mfma<T>::mma(a, bq, sacc[kt]);
+          // the first instruction of each tile starts from a zero accumulator
+          sacc[kt] = Mfma<T>::mma(a, bq, (s == 0 && u == 0) ? f32x16{} : sacc[kt]);
         }
       }
     }

@@ -70,18 +70,58 @@ __global__ __launch_bounds__(256) void k_ln_mod(const float* __restrict__ h, int
   const int lane = threadIdx.x & 63;
   if (row >= rows) return;
   const float* hr = h + (size_t)row * D;
-  float v[NPL];
-#pragma unroll
-  for (int j = 0; j < NPL; ++j) v[j] = hr[lane + 64 * j];
-  float mean, rstd;
-  row_stats<NPL>(v, mean, rstd);
   T* o = out + (size_t)row * D;
+  if constexpr (NPL % 4 == 0) {
+    // 16-byte loads: lane owns elements 4*(lane + 64 j) .. +3.
+    constexpr int NV = NPL / 4;
+    float4 v[NV];
 #pragma unroll
-  for (int j = 0; j < NPL; ++j) {
-    const int n = lane + 64 * j;
-    float u = (v[j] - mean) * rstd;
-    if (scale) u = u * (1.0f + scale[n]) + shift[n];
-    o[n] = from_f32<T>(u);
+    for (int j = 0; j < NV; ++j) v[j] = reinterpret_cast<const float4*>(hr)[lane + 64 * j];
+    float sum = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) sum += (v[j].x + v[j].y) + (v[j].z + v[j].w);
+    const float mean = wave_sum(sum) * (1.0f / D);
+    float sq = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      const float a = v[j].x - mean, b = v[j].y - mean, c = v[j].z - mean, d = v[j].w - mean;
+      sq += (a * a + b * b) + (c * c + d * d);
+    }
+    const float rstd = rsqrtf(wave_sum(sq) * (1.0f / D) + kLnEps);
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      const int n = 4 * (lane + 64 * j);
+      float u[4] = {(v[j].x - mean) * rstd, (v[j].y - mean) * rstd, (v[j].z - mean) * rstd, (v[j].w - mean) * rstd};
+      if (scale) {
+        const float4 sc = *reinterpret_cast<const float4*>(scale + n);
+        const float4 sh = *reinterpret_cast<const float4*>(shift + n);
+        u[0] = u[0] * (1.0f + sc.x) + sh.x;
+        u[1] = u[1] * (1.0f + sc.y) + sh.y;
+        u[2] = u[2] * (1.0f + sc.z) + sh.z;
+        u[3] = u[3] * (1.0f + sc.w) + sh.w;
+      }
+      if constexpr (sizeof(T) == 2) {
+        bf16x4 w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[e] = (bf16)u[e];
+        *reinterpret_cast<bf16x4*>(o + n) = w;
+      } else {
+        *reinterpret_cast<float4*>(o + n) = make_float4(u[0], u[1], u[2], u[3]);
+      }
+    }
+  } else {
+    float v[NPL];
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) v[j] = hr[lane + 64 * j];
+    float mean, rstd;
+    row_stats<NPL>(v, mean, rstd);
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) {
+      const int n = lane + 64 * j;
+      float u = (v[j] - mean) * rstd;
+      if (scale) u = u * (1.0f + scale[n]) + shift[n];
+      o[n] = from_f32<T>(u);
+    }
   }
 }
 
