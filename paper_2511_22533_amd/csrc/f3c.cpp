@@ -209,9 +209,8 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
     Scope sc(s, F3C_PROF_MOD, st, 0, (double)es * d * (256 + d + 6.0 * L * d));
     const char* mw = m->wdev;
     HIP_TRY(launch_gemv(dt, m->w("t1_w"), m->b("t1_b"), nullptr, t, GEMV_IN_TIMESTEP, 1, d, 256, s->temb, st));
-    HIP_TRY(launch_gemv(dt, m->w("t2_w"), m->b("t2_b"), s->temb, 0.0, GEMV_IN_PLAIN, 1, d, d, s->temb + d, st));
-    HIP_TRY(launch_gemv(dt, mw + m->mod_w, (const float*)(mw + m->mod_b), s->temb + d, 0.0, GEMV_IN_PLAIN, 0,
-                        6 * L * d, d, s->mod, st));
+    HIP_TRY(launch_gemv(dt, m->w("t2_w"), m->b("t2_b"), s->temb, 0.0, GEMV_IN_PLAIN, 0, d, d, s->temb + d, st));
+    HIP_TRY(launch_gemv_t(dt, mw + m->mod_w, (const float*)(mw + m->mod_b), s->temb + d, 6 * L * d, d, s->mod, st));
   }
   if (rows > 0) {
     {
@@ -408,9 +407,27 @@ int f3c_model_load_weights(f3c_model* m, void* weights_dev, size_t bytes, const 
     if (!host_f32[i]) return fail(F3C_EINVAL, "weight %s is NULL", m->specs[i].name.c_str());
   std::vector<char> stage;
   char* dev = static_cast<char*>(weights_dev);
+  // All blocks' modulation weights are stored input-major, [d][L*6d], for the
+  // streaming GEMV; the other matrices keep their [out][in] layout.
+  const int64_t d = m->d, R = (int64_t)m->L * 6 * d;
+  std::vector<char> modt((size_t)(R * d) * m->es);
   for (int32_t i = 0; i < n; ++i) {
     const Spec& s = m->specs[i];
     const int64_t ne = s.numel();
+    const size_t dot = s.name.find('.');
+    if (dot != std::string::npos && s.name.substr(dot + 1) == "mod_w") {
+      const int64_t l = std::stoll(s.name.substr(3, dot - 3));
+      for (int64_t r = 0; r < 6 * d; ++r)
+        for (int64_t k = 0; k < d; ++k) {
+          const float v = host_f32[i][r * d + k];
+          const size_t o = (size_t)(k * R + l * 6 * d + r);
+          if (m->es == 2)
+            reinterpret_cast<uint16_t*>(modt.data())[o] = f32_to_bf16_bits(v);
+          else
+            reinterpret_cast<float*>(modt.data())[o] = v;
+        }
+      continue;
+    }
     if (s.bias || m->es == 4) {
       HIP_TRY(hipMemcpy(dev + s.off, host_f32[i], (size_t)ne * 4, hipMemcpyHostToDevice));
     } else {
@@ -420,6 +437,7 @@ int f3c_model_load_weights(f3c_model* m, void* weights_dev, size_t bytes, const 
       HIP_TRY(hipMemcpy(dev + s.off, stage.data(), (size_t)ne * 2, hipMemcpyHostToDevice));
     }
   }
+  HIP_TRY(hipMemcpy(dev + m->mod_w, modt.data(), modt.size(), hipMemcpyHostToDevice));
   m->wdev = dev;
   m->loaded = true;
   return F3C_OK;
@@ -726,9 +744,9 @@ int f3c_op_modulation(const f3c_model* m, double t, float* mod_dev, float* scrat
   hipStream_t st = (hipStream_t)stream;
   const int d = m->d, dt = m->cfg.dtype;
   HIP_TRY(launch_gemv(dt, m->w("t1_w"), m->b("t1_b"), nullptr, t, GEMV_IN_TIMESTEP, 1, d, 256, scratch_dev, st));
-  HIP_TRY(launch_gemv(dt, m->w("t2_w"), m->b("t2_b"), scratch_dev, 0.0, GEMV_IN_PLAIN, 1, d, d, scratch_dev + d, st));
-  HIP_TRY(launch_gemv(dt, m->wdev + m->mod_w, (const float*)(m->wdev + m->mod_b), scratch_dev + d, 0.0,
-                      GEMV_IN_PLAIN, 0, 6 * m->L * d, d, mod_dev, st));
+  HIP_TRY(launch_gemv(dt, m->w("t2_w"), m->b("t2_b"), scratch_dev, 0.0, GEMV_IN_PLAIN, 0, d, d, scratch_dev + d, st));
+  HIP_TRY(launch_gemv_t(dt, m->wdev + m->mod_w, (const float*)(m->wdev + m->mod_b), scratch_dev + d, 6 * m->L * d, d,
+                        mod_dev, st));
   return F3C_OK;
 }
 

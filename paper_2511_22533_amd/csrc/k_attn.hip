@@ -200,7 +200,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
       for (int e = 0; e < 16; ++e) {
         const float pe = __builtin_amdgcn_exp2f(fmaf(sacc[kt][e], c, -mc));
         sacc[kt][e] = pe;
-        l_run += pe;
+        if constexpr (ES == 4) l_run += pe;
       }
 
     // O^T += V^T P^T over the 64 keys.
@@ -212,6 +212,12 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
         if constexpr (ES == 2) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) pf[e] = (bf16)sacc[kt][8 * u + e];
+          // Row sum of the probabilities as rounded for the PV product (v_dot2 with 1s).
+          const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
+          l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf, pf, 0, 1), ones, l_run, false);
+          l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf, pf, 2, 3), ones, l_run, false);
+          l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf, pf, 4, 5), ones, l_run, false);
+          l_run = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pf, pf, 6, 7), ones, l_run, false);
         } else {
           pf = sacc[kt][u];
         }

@@ -59,7 +59,7 @@ __device__ __forceinline__ void store4<bf16>(bf16* dst, const float (&v)[4]) {
   *reinterpret_cast<bf16x4*>(dst) = o;
 }
 
-template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, int EPI, int SITE>
+template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, int EPI, int SITE, int PF = 1>
 __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs p) {
   constexpr int NT = 64 * WGM * WGN;                        // threads
   constexpr int WTM = BM / WGM, WTN = BN / WGN;             // wave tile
@@ -98,21 +98,22 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs p) {
     chunk_b[q] = row * kRS + (c & 7) * 16;
   }
 
-  u32x4 ra[CA], rb[CB];
-  auto load_tile = [&](int kt) {
+  // PF register sets: set r holds the tile whose index is congruent to r mod PF.
+  u32x4 ra[PF][CA], rb[PF][CB];
+  auto load_tile = [&](int kt, int r) {
     const size_t kb = (size_t)kt * kBKB;
 #pragma unroll
-    for (int q = 0; q < CA; ++q) ra[q] = *reinterpret_cast<const u32x4*>(a_row[q] + kb);
+    for (int q = 0; q < CA; ++q) ra[r][q] = *reinterpret_cast<const u32x4*>(a_row[q] + kb);
 #pragma unroll
-    for (int q = 0; q < CB; ++q) rb[q] = *reinterpret_cast<const u32x4*>(w_row[q] + kb);
+    for (int q = 0; q < CB; ++q) rb[r][q] = *reinterpret_cast<const u32x4*>(w_row[q] + kb);
   };
-  auto store_tile = [&](int buf) {
+  auto store_tile = [&](int buf, int r) {
     char* As = lds + buf * (ABUF + BBUF);
     char* Bs = As + ABUF;
 #pragma unroll
-    for (int q = 0; q < CA; ++q) *reinterpret_cast<u32x4*>(As + chunk_a[q]) = ra[q];
+    for (int q = 0; q < CA; ++q) *reinterpret_cast<u32x4*>(As + chunk_a[q]) = ra[r][q];
 #pragma unroll
-    for (int q = 0; q < CB; ++q) *reinterpret_cast<u32x4*>(Bs + chunk_b[q]) = rb[q];
+    for (int q = 0; q < CB; ++q) *reinterpret_cast<u32x4*>(Bs + chunk_b[q]) = rb[r][q];
   };
 
   f32x16 acc[TM][TN];
@@ -154,22 +155,47 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs p) {
     }
   };
 
-  load_tile(0);
-  store_tile(0);
-  __syncthreads();
-  for (int kt = 0; kt < KT; ++kt) {
-    if (kt + 1 < KT) load_tile(kt + 1);
-    if constexpr (STAGES == 2) {
-      compute(kt & 1);
-      if (kt + 1 < KT) store_tile((kt + 1) & 1);
-      __syncthreads();
-    } else {
-      compute(0);
-      __syncthreads();
-      if (kt + 1 < KT) {
-        store_tile(0);
+  if constexpr (PF == 1) {
+    load_tile(0, 0);
+    store_tile(0, 0);
+    __syncthreads();
+    for (int kt = 0; kt < KT; ++kt) {
+      if (kt + 1 < KT) load_tile(kt + 1, 0);
+      if constexpr (STAGES == 2) {
+        compute(kt & 1);
+        if (kt + 1 < KT) store_tile((kt + 1) & 1, 0);
         __syncthreads();
+      } else {
+        compute(0);
+        __syncthreads();
+        if (kt + 1 < KT) {
+          store_tile(0, 0);
+          __syncthreads();
+        }
       }
+    }
+  } else {
+    // Prefetch distance PF (2 or 3) with double-buffered LDS: at step kt the
+    // loads of tile kt+PF are issued while tile kt is consumed and tile kt+1
+    // (loaded PF-1 steps earlier) is staged. Loads are issued unconditionally
+    // (past the end they re-read the last tile), so the wait before staging
+    // only covers the oldest load group.
+    static_assert(STAGES == 2 && PF <= 3, "prefetch distance 2-3 needs two LDS buffers");
+#pragma unroll
+    for (int r = 0; r < PF; ++r) load_tile(min(r, KT - 1), r);
+    store_tile(0, 0);
+    __syncthreads();
+    auto step = [&](int kt, int rr, int rl) {   // rr = kt % PF, rl = kt % 2 (constants below)
+      load_tile(min(kt + PF, KT - 1), rr);
+      compute(rl);
+      store_tile(rl ^ 1, rr + 1 == PF ? 0 : rr + 1);
+      __syncthreads();
+    };
+    constexpr int U = PF == 3 ? 6 : 2;
+    for (int kt = 0; kt < KT; kt += U) {
+#pragma unroll
+      for (int i = 0; i < U; ++i)
+        if (kt + i < KT) step(kt + i, i % PF, i & 1);
     }
   }
 
@@ -251,10 +277,10 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(GemmArgs p, const float* 
   }
 }
 
-template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, int EPI, int SITE>
+template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, int EPI, int SITE, int PF = 1>
 hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
   dim3 grid(a.N / BN, (a.M + BM - 1) / BM);
-  hipLaunchKernelGGL((k_gemm<T, BM, BN, WGM, WGN, STAGES, EPI, SITE>), grid, dim3(64 * WGM * WGN), 0, s, a);
+  hipLaunchKernelGGL((k_gemm<T, BM, BN, WGM, WGN, STAGES, EPI, SITE, PF>), grid, dim3(64 * WGM * WGN), 0, s, a);
   return hipGetLastError();
 }
 
@@ -264,7 +290,7 @@ hipError_t launch_splitk(const GemmArgs& a, int splits, float* ws, hipStream_t s
   GemmArgs pa = a;
   pa.resid = ws;
   dim3 grid(a.N / 64, (a.M + 63) / 64, splits);
-  hipLaunchKernelGGL((k_gemm<T, 64, 64, 2, 2, 2, EPI_PARTIAL, SITE>), grid, dim3(256), 0, s, pa);
+  hipLaunchKernelGGL((k_gemm<T, 64, 64, 2, 2, 2, EPI_PARTIAL, SITE, 2>), grid, dim3(256), 0, s, pa);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t total4 = (int64_t)a.M * a.N / 4;
@@ -273,25 +299,46 @@ hipError_t launch_splitk(const GemmArgs& a, int splits, float* ws, hipStream_t s
   return hipGetLastError();
 }
 
-// Tile choice (measured on MI355X at M = 820 ... 4096, N = 1024 ... 4096):
-// 128 x 128 with 8 waves while that gives >= 2 workgroups per CU, else 64 x 128
-// single-buffered, else 64 x 64; long-K shapes with few 64 x 64 tiles are split
-// along K when a workspace is available.
+// Tile choice for bf16 (fitted to measurements on MI355X at M = 820 ... 4096,
+// N = 1024 ... 4096, K = 1024 / 4096): estimated time = rounds of 256
+// workgroups x per-tile work / relative per-tile efficiency, with
+// 128 x 128 (8 waves) = 1, 64 x 128 = 0.72, 64 x 64 = 0.77. Long-K shapes that
+// fit in one round of 64 x 64 tiles are split in two along K when a workspace
+// is available (measured: two slices beat one and four at M = 820 ... 1310).
+struct TileChoice {
+  int cfg;       // 0: 128x128, 1: 64x128, 2: 64x64
+  int splits;
+};
+
+inline TileChoice choose_tiles(int M, int N, int K, int es, size_t ws_bytes) {
+  auto rounds = [&](int bm, int bn) { return (((long)(M + bm - 1) / bm) * (N / bn) + 255) / 256; };
+  const double c128 = rounds(128, 128) * 16384.0;
+  const double c64x128 = rounds(64, 128) * 8192.0 / 0.72;
+  const double c64 = rounds(64, 64) * 4096.0 / 0.77;
+  TileChoice t{0, 1};
+  double best = c128;
+  if (c64x128 < best) { best = c64x128; t.cfg = 1; }
+  if (c64 < best) { best = c64; t.cfg = 2; }
+  const long t64 = ((long)(M + 63) / 64) * (N / 64);
+  const int kt = K * es / kBKB;
+  if (t.cfg == 2 && t64 <= 256 && kt >= 32) {
+    int splits = 1;
+    while (splits < 2 && t64 * splits * 2 <= 1024 && kt % (2 * splits) == 0) splits *= 2;
+    if ((size_t)splits * M * N * sizeof(float) <= ws_bytes) t.splits = splits;
+  }
+  return t;
+}
+
 template <typename T, int EPI, int SITE>
 hipError_t launch_t(const GemmArgs& a, float* ws, size_t ws_bytes, hipStream_t s) {
-  auto tiles = [&](int bm, int bn) { return (long)((a.M + bm - 1) / bm) * (a.N / bn); };
   if constexpr (sizeof(T) == 2) {
-    if (tiles(128, 128) >= 512) return launch_cfg<T, 128, 128, 2, 4, 2, EPI, SITE>(a, s);
-    if (tiles(64, 128) >= 512) return launch_cfg<T, 64, 128, 2, 2, 1, EPI, SITE>(a, s);
-    const long t64 = tiles(64, 64);
-    const int kt = a.K * (int)sizeof(T) / kBKB;
-    int splits = 1;
-    while (splits < 4 && t64 * splits < 512 && kt % (2 * splits) == 0 && kt / (2 * splits) >= 8) splits *= 2;
-    if (splits > 1 && ws && (size_t)splits * a.M * a.N * sizeof(float) <= ws_bytes)
-      return launch_splitk<T, EPI, SITE>(a, splits, ws, s);
-    return launch_cfg<T, 64, 64, 2, 2, 2, EPI, SITE>(a, s);
+    const TileChoice t = choose_tiles(a.M, a.N, a.K, sizeof(T), ws ? ws_bytes : 0);
+    if (t.splits > 1) return launch_splitk<T, EPI, SITE>(a, t.splits, ws, s);
+    if (t.cfg == 0) return launch_cfg<T, 128, 128, 2, 4, 2, EPI, SITE, 2>(a, s);
+    if (t.cfg == 1) return launch_cfg<T, 64, 128, 2, 2, 2, EPI, SITE, 2>(a, s);
+    return launch_cfg<T, 64, 64, 2, 2, 2, EPI, SITE, 2>(a, s);
   } else {
-    return launch_cfg<T, 64, 128, 2, 2, 2, EPI, SITE>(a, s);
+    return launch_cfg<T, 64, 128, 2, 2, 2, EPI, SITE, 2>(a, s);
   }
 }
 

@@ -243,6 +243,54 @@ __global__ __launch_bounds__(256) void k_gemv(const T* __restrict__ W, const flo
   }
 }
 
+// y[r] = sum_k Wt[k][r] SiLU(x[k]) + b[r] for a weight stored input-major
+// (Wt [K][R]). Lane owns 16/sizeof(T) consecutive outputs and streams 16-byte
+// rows of Wt, so no cross-lane reduction is needed; the 4 waves of a
+// workgroup split K and combine their partial sums through LDS.
+template <typename T>
+__global__ __launch_bounds__(256) void k_gemv_t(const T* __restrict__ Wt, const float* __restrict__ bias,
+                                                const float* __restrict__ x, int R, int K, float* __restrict__ y) {
+  constexpr int V = 16 / sizeof(T);
+  __shared__ float part[3][64 * V];
+  __shared__ float xs[4096];
+  for (int k = threadIdx.x; k < K; k += 256) xs[k] = silu(x[k]);
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r0 = blockIdx.x * 64 * V + lane * V;
+  const int kq = K / 4, k0 = wave * kq;
+  float acc[V];
+#pragma unroll
+  for (int e = 0; e < V; ++e) acc[e] = 0.0f;
+  if (r0 < R) {
+    const T* w = Wt + (size_t)k0 * R + r0;
+#pragma unroll 8
+    for (int k = 0; k < kq; ++k) {
+      const float xv = xs[k0 + k];
+      if constexpr (sizeof(T) == 2) {
+        const bf16x8 wv = *reinterpret_cast<const bf16x8*>(w + (size_t)k * R);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] += (float)wv[e] * xv;
+      } else {
+        const float4 wv = *reinterpret_cast<const float4*>(w + (size_t)k * R);
+        acc[0] += wv.x * xv;
+        acc[1] += wv.y * xv;
+        acc[2] += wv.z * xv;
+        acc[3] += wv.w * xv;
+      }
+    }
+  }
+  if (wave > 0) {
+#pragma unroll
+    for (int e = 0; e < V; ++e) part[wave - 1][lane * V + e] = acc[e];
+  }
+  __syncthreads();
+  if (wave == 0 && r0 < R) {
+#pragma unroll
+    for (int e = 0; e < V; ++e)
+      y[r0 + e] = ((acc[e] + part[0][lane * V + e]) + (part[1][lane * V + e] + part[2][lane * V + e])) + bias[r0 + e];
+  }
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void k_convert(const float* __restrict__ src, T* __restrict__ dst, int64_t n) {
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
@@ -310,6 +358,17 @@ hipError_t launch_gemv(int dt, const void* W, const float* bias, const float* x,
   else
     hipLaunchKernelGGL(k_gemv<float>, grid, dim3(256), lds, s, (const float*)W, bias, x, t, in_mode, out_silu,
                        rows, K, y);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemv_t(int dt, const void* Wt, const float* bias, const float* x, int R, int K, float* y,
+                         hipStream_t s) {
+  const int per_block = 64 * (dt == DT_BF16 ? 8 : 4);
+  dim3 grid((R + per_block - 1) / per_block);
+  if (dt == DT_BF16)
+    hipLaunchKernelGGL(k_gemv_t<bf16>, grid, dim3(256), 0, s, (const bf16*)Wt, bias, x, R, K, y);
+  else
+    hipLaunchKernelGGL(k_gemv_t<float>, grid, dim3(256), 0, s, (const float*)Wt, bias, x, R, K, y);
   return hipGetLastError();
 }
 

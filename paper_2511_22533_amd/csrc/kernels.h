@@ -56,6 +56,11 @@ enum GemvIn { GEMV_IN_PLAIN = 0, GEMV_IN_SILU = 1, GEMV_IN_TIMESTEP = 2 };
 hipError_t launch_gemv(int dt, const void* W, const float* bias, const float* x, double t, int in_mode,
                        int out_silu, int rows, int K, float* y, hipStream_t s);
 
+// y[r] = sum_k Wt[k][r] SiLU(x[k]) + b[r] with the weight stored input-major
+// (Wt [K][R]); R a multiple of 16 / sizeof(element), K a multiple of 4, K <= 4096.
+hipError_t launch_gemv_t(int dt, const void* Wt, const float* bias, const float* x, int R, int K, float* y,
+                         hipStream_t s);
+
 // Element type conversion f32 -> model dtype.
 hipError_t launch_convert(int dt, const float* src, void* dst, int64_t n, hipStream_t s);
 
