@@ -47,6 +47,9 @@ def parse():
     ap.add_argument("--workload", default="trellis16_cached")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-depth", type=int, default=8, help="oracle blocks timed (0 = full depth)")
+    ap.add_argument("--copy-ref-mb", type=int, default=0,
+                    help="first run one plain device-to-device copy of this many MiB (a known-size reference "
+                         "for hardware byte counters)")
     return ap.parse_args()
 
 
@@ -117,6 +120,14 @@ def main():
     cfg = w.model
     torch.cuda.set_device(0)
     print(f"[bench] workload {w.name}: {w.description}", file=sys.stderr, flush=True)
+    if args.copy_ref_mb:
+        src = torch.ones(args.copy_ref_mb << 18, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"[bench] reference copy of {args.copy_ref_mb} MiB done", file=sys.stderr, flush=True)
+        del src, dst
     W = synth.make_weights(cfg)
     cond = synth.make_cond(cfg, w.batch)
     x_T = synth.make_noise(cfg, w.batch)

@@ -59,6 +59,16 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// Workgroups are dispatched round-robin over the 8 XCDs (each with its own
+// L2). Map the hardware workgroup id to a logical id so that each XCD receives
+// one contiguous range of logical ids (sizes differ by at most one).
+__device__ __forceinline__ int xcd_logical_id(int hw, int total) {
+  constexpr int kXcd = 8;
+  const int x = hw % kXcd, i = hw / kXcd;
+  const int q = total / kXcd, r = total % kXcd;
+  return x * q + (x < r ? x : r) + i;
+}
+
 // Sample lookup in a segment table off[0..B] (off[B] = total rows).
 __device__ __forceinline__ int find_segment(const int* off, int B, int row) {
   int b = 0;

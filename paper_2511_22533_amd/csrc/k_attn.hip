@@ -35,6 +35,7 @@ struct AttnArgs {
   const char* v;
   char* o;
   int ldq, ldk, ldv, ldo;        // elements
+  int heads;
   float scale_log2;              // log2(e) / sqrt(hd)
 };
 
@@ -60,9 +61,13 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 5, r32 = lane & 31;
-  const int head = blockIdx.y;
-  const int b = find_segment(p.tile_off, p.qs.B, blockIdx.x);
-  const int qt = blockIdx.x - p.tile_off[b];
+  // 1-D grid over (head, query tile); all tiles of a head share one XCD's L2.
+  const int ntq = p.tile_off[p.qs.B];
+  const int logical = xcd_logical_id(blockIdx.x, ntq * p.heads);
+  const int head = logical / ntq;
+  const int tq = logical - head * ntq;
+  const int b = find_segment(p.tile_off, p.qs.B, tq);
+  const int qt = tq - p.tile_off[b];
   const int q_begin = p.qs.off[b], nq = p.qs.off[b + 1] - q_begin;
   const int k_begin = p.ks.off[b], nk = p.ks.off[b + 1] - k_begin;
   const int qi = qt * BQ + wave * 32 + r32;            // query of this lane (within the sample)
@@ -79,14 +84,15 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
 
   // Tile staging: K row-major, V transposed (pairs of keys per 32/64-bit write).
   // Keys past the end are read from the last key (always valid) and masked.
-  u32x4 rk[KCH], rv[VPR][2];
-  auto fetch = [&](int kv0) {
+  // Two register sets: tile t+2 is fetched while tile t+1 waits to be staged.
+  u32x4 rk[2][KCH], rv[2][VPR][2];
+  auto fetch = [&](int kv0, int r) {
 #pragma unroll
     for (int q = 0; q < KCH; ++q) {
       const int ch = tid + NT * q, row = ch / CPR, col = ch % CPR;
       if (KITEMS % NT != 0 && ch >= KITEMS) break;
       const int key = min(kv0 + row, nk - 1);
-      rk[q] = *reinterpret_cast<const u32x4*>(p.k + ((size_t)(k_begin + key) * p.ldk + head * HD) * ES + col * 16);
+      rk[r][q] = *reinterpret_cast<const u32x4*>(p.k + ((size_t)(k_begin + key) * p.ldk + head * HD) * ES + col * 16);
     }
 #pragma unroll
     for (int q = 0; q < VPR; ++q) {
@@ -95,25 +101,25 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const int key = min(kv0 + 2 * pr + h, nk - 1);
-        rv[q][h] = *reinterpret_cast<const u32x4*>(p.v + ((size_t)(k_begin + key) * p.ldv + head * HD) * ES + col * 16);
+        rv[r][q][h] = *reinterpret_cast<const u32x4*>(p.v + ((size_t)(k_begin + key) * p.ldv + head * HD) * ES + col * 16);
       }
     }
   };
-  auto stage = [&](int buf) {
+  auto stage = [&](int buf, int r) {
     char* Ks = lds + buf * (KBUF + VBUF);
     char* Vt = Ks + KBUF;
 #pragma unroll
     for (int q = 0; q < KCH; ++q) {
       const int ch = tid + NT * q, row = ch / CPR, col = ch % CPR;
       if (KITEMS % NT != 0 && ch >= KITEMS) break;
-      *reinterpret_cast<u32x4*>(Ks + row * KRS + col * 16) = rk[q];
+      *reinterpret_cast<u32x4*>(Ks + row * KRS + col * 16) = rk[r][q];
     }
 #pragma unroll
     for (int q = 0; q < VPR; ++q) {
       const int it = tid + NT * q, pr = it / CPR, col = it % CPR;
       if (VITEMS % NT != 0 && it >= VITEMS) break;
-      const T* v0 = reinterpret_cast<const T*>(&rv[q][0]);
-      const T* v1 = reinterpret_cast<const T*>(&rv[q][1]);
+      const T* v0 = reinterpret_cast<const T*>(&rv[r][q][0]);
+      const T* v1 = reinterpret_cast<const T*>(&rv[r][q][1]);
 #pragma unroll
       for (int e = 0; e < PER16; ++e) {
         char* dst = Vt + (col * PER16 + e) * VRS + 2 * pr * ES;
@@ -136,13 +142,16 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
   const float c = p.scale_log2;
   const int ntiles = (nk + kBKV - 1) / kBKV;
 
-  fetch(0);
-  stage(0);
+  // Fetches are unconditional (past the end they re-read the last tile), so the
+  // wait before staging tile t+1 does not cover the loads of tile t+2.
+  fetch(0, 0);
+  fetch(min(kBKV, (ntiles - 1) * kBKV), 1);
+  stage(0, 0);
   __syncthreads();
-  for (int t = 0; t < ntiles; ++t) {
+  auto tile = [&](int t, int r) {        // r = t & 1 (a constant at each call site)
     const int kv0 = t * kBKV;
-    if (t + 1 < ntiles) fetch(kv0 + kBKV);
-    const char* Ks = lds + (t & 1) * (KBUF + VBUF);
+    fetch(min(kv0 + 2 * kBKV, (ntiles - 1) * kBKV), r);
+    const char* Ks = lds + r * (KBUF + VBUF);
     const char* Vt = Ks + KBUF;
 
     // S^T tiles: rows = keys kv0 + 32*kt + ..., cols = this wave's 32 queries.
@@ -237,9 +246,15 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
           oacc[h] = Mfma<T>::mma(vf, pf, oacc[h]);
         }
       }
-    if (t + 1 < ntiles) stage((t + 1) & 1);
+    stage(r ^ 1, r ^ 1);
     __syncthreads();
+  };
+  int t = 0;
+  for (; t + 1 < ntiles; t += 2) {
+    tile(t, 0);
+    tile(t + 1, 1);
   }
+  if (t < ntiles) tile(t, 0);
 
   if (!q_ok) return;
   const float l_tot = l_run + __shfl_xor(l_run, 32);
@@ -272,7 +287,8 @@ hipError_t launch_a(int dt, int hd, const AttnArgs& a0, int heads, hipStream_t s
   for (int b = 0; b < a.qs.B; ++b) a.tile_off[b + 1] = a.tile_off[b] + (a.qs.off[b + 1] - a.qs.off[b] + BQ - 1) / BQ;
   const int tiles = a.tile_off[a.qs.B];
   if (tiles == 0) return hipSuccess;
-  dim3 grid(tiles, heads), block(64 * NW);
+  a.heads = heads;
+  dim3 grid(tiles * heads), block(64 * NW);
   if (dt == DT_BF16 && hd == 64) hipLaunchKernelGGL((k_attn<bf16, 64, NW, SITE>), grid, block, 0, s, a);
   else if (dt == DT_BF16 && hd == 32) hipLaunchKernelGGL((k_attn<bf16, 32, NW, SITE>), grid, block, 0, s, a);
   else if (dt == DT_F32 && hd == 64) hipLaunchKernelGGL((k_attn<float, 64, NW, SITE>), grid, block, 0, s, a);
