@@ -205,10 +205,16 @@ int f3c_op_gemm(int32_t dtype, int32_t epilogue, int32_t M, int32_t N, int32_t K
 /* Varlen multi-head attention: sample b's queries are rows q_off[b]..q_off[b+1]
  * of q (T, row stride ldq), its keys/values rows k_off[b]..k_off[b+1] of k/v;
  * head h uses columns h*head_dim..; o (T) gets one row per query.
- * head_dim in {32, 64}; offsets are host arrays of B+1 non-decreasing ints. */
+ * head_dim in {32, 64}; offsets are host arrays of B+1 non-decreasing ints.
+ * workspace (device, 16-byte aligned, may be NULL) lets launches with few
+ * query tiles split the key range: each split's unnormalised output, max and
+ * sum go to the workspace (splits * rows * heads * (head_dim + 2) floats) and
+ * are merged in split order, so results do not depend on scheduling. The
+ * split count shrinks to what the workspace holds. */
 int f3c_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int32_t batch, const int32_t* q_off_host,
                      const int32_t* k_off_host, const void* q, int32_t ldq, const void* k, int32_t ldk,
-                     const void* v, int32_t ldv, void* o, int32_t ldo, f3c_stream stream);
+                     const void* v, int32_t ldv, void* o, int32_t ldo, float* workspace, size_t workspace_bytes,
+                     f3c_stream stream);
 
 /* out T [rows][d] = LN(h) * (1 + scale) + shift (no affine LN, eps 1e-6);
  * shift/scale f32 [d] or both NULL. d in {128, 256, 512, 1024, 2048}. */

@@ -237,7 +237,7 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
         Scope sc(s, F3C_PROF_ATTN_SELF, st, fl, 0);
         const char* q = static_cast<const char*>(s->qkv);
         HIP_TRY(launch_attention(SITE_SELF, dt, m->cfg.heads, m->hd, act, act, q, 3 * d, q + d * es, 3 * d, q + 2 * d * es,
-                                 3 * d, s->att, d, st));
+                                 3 * d, s->att, d, s->ws, s->ws_bytes, st));
       }
       {
         Scope sc(s, F3C_PROF_GEMM_O, st, 2.0 * rows * d * d, 0);
@@ -257,7 +257,7 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
         Scope sc(s, F3C_PROF_ATTN_CROSS, st, 4.0 * rows * m->Nc * d, 0);
         const char* kv = static_cast<const char*>(s->kv) + (size_t)l * 2 * d * es;
         HIP_TRY(launch_attention(SITE_CROSS, dt, m->cfg.heads, m->hd, act, cond_segs, s->qc, d, kv, 2 * L * d, kv + d * es,
-                                 2 * L * d, s->att, d, st));
+                                 2 * L * d, s->att, d, s->ws, s->ws_bytes, st));
       }
       {
         Scope sc(s, F3C_PROF_GEMM_CO, st, 2.0 * rows * d * d, 0);
@@ -702,7 +702,8 @@ int f3c_op_gemm(int32_t dtype, int32_t epilogue, int32_t M, int32_t N, int32_t K
 
 int f3c_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int32_t batch, const int32_t* q_off_host,
                      const int32_t* k_off_host, const void* q, int32_t ldq, const void* k, int32_t ldk,
-                     const void* v, int32_t ldv, void* o, int32_t ldo, f3c_stream stream) {
+                     const void* v, int32_t ldv, void* o, int32_t ldo, float* workspace, size_t workspace_bytes,
+                     f3c_stream stream) {
   if (dtype != F3C_F32 && dtype != F3C_BF16) return fail(F3C_EINVAL, "bad dtype");
   if (head_dim != 32 && head_dim != 64) return fail(F3C_EINVAL, "head_dim must be 32 or 64");
   if (heads < 1 || heads > 65535) return fail(F3C_EINVAL, "bad heads");
@@ -723,7 +724,9 @@ int f3c_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int32_t bat
   for (int b = 0; b < batch; ++b)
     if (qs.off[b + 1] > qs.off[b] && ks.off[b + 1] == ks.off[b])
       return fail(F3C_EINVAL, "sample %d has queries but no keys", b);
-  HIP_TRY(launch_attention(SITE_OP, dtype, heads, head_dim, qs, ks, q, ldq, k, ldk, v, ldv, o, ldo, (hipStream_t)stream));
+  if (workspace && ((uintptr_t)workspace & 15)) return fail(F3C_EINVAL, "workspace must be 16-byte aligned");
+  HIP_TRY(launch_attention(SITE_OP, dtype, heads, head_dim, qs, ks, q, ldq, k, ldk, v, ldv, o, ldo, workspace,
+                           workspace ? workspace_bytes : 0, (hipStream_t)stream));
   return F3C_OK;
 }
 

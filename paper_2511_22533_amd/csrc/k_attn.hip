@@ -17,6 +17,13 @@
 // lazily: the accumulators are rescaled only when some query's max grows by
 // more than 2^8 (in base-2 units), which keeps every unnormalised probability
 // below 2^8 and the result unchanged up to rounding.
+//
+// Few query tiles (late cached steps: a few hundred active tokens) cannot fill
+// 256 CUs, so the key range may be split: each split writes its unnormalised
+// output with its reference max and sum in f32, and a second kernel merges the
+// splits in split order (the standard log-sum-exp combination; deterministic).
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -37,9 +44,13 @@ struct AttnArgs {
   int ldq, ldk, ldv, ldo;        // elements
   int heads;
   float scale_log2;              // log2(e) / sqrt(hd)
+  int splits;                    // key-range splits (1: normalised output straight to o)
+  int rows;                      // query rows qs.off[B] - qs.off[0] (split partials)
+  float* part_o;                 // [splits][rows][heads][hd] unnormalised outputs
+  float* part_ml;                // [splits][rows][heads][2] (max * scale_log2, sum)
 };
 
-template <typename T, int HD, int NW, int SITE>
+template <typename T, int HD, int NW, int SITE, bool SPLIT>
 __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
   constexpr int NT = 64 * NW;
   constexpr int BQ = 32 * NW;
@@ -61,11 +72,13 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 5, r32 = lane & 31;
-  // 1-D grid over (head, query tile); all tiles of a head share one XCD's L2.
+  // 1-D grid over (head, query tile, split); all work of a head shares one XCD's L2.
   const int ntq = p.tile_off[p.qs.B];
-  const int logical = xcd_logical_id(blockIdx.x, ntq * p.heads);
-  const int head = logical / ntq;
-  const int tq = logical - head * ntq;
+  const int nsp = SPLIT ? p.splits : 1;
+  const int logical = xcd_logical_id(blockIdx.x, ntq * p.heads * nsp);
+  const int head = logical / (ntq * nsp);
+  const int rem = logical - head * ntq * nsp;
+  const int tq = rem / nsp, sp = rem - tq * nsp;
   const int b = find_segment(p.tile_off, p.qs.B, tq);
   const int qt = tq - p.tile_off[b];
   const int q_begin = p.qs.off[b], nq = p.qs.off[b + 1] - q_begin;
@@ -140,17 +153,17 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
     for (int e = 0; e < 16; ++e) oacc[t][e] = 0.0f;
   float m_run = -INFINITY, l_run = 0.0f;       // running max (raw logits), unnormalised sum
   const float c = p.scale_log2;
+  // Key tiles [t_begin, t_end) of this split (balanced; empty when the sample
+  // has fewer tiles than splits).
   const int ntiles = (nk + kBKV - 1) / kBKV;
+  const int t_begin = sp * ntiles / nsp, t_end = (sp + 1) * ntiles / nsp;
+  const int last_kv = (t_end - 1) * kBKV;
 
   // Fetches are unconditional (past the end they re-read the last tile), so the
   // wait before staging tile t+1 does not cover the loads of tile t+2.
-  fetch(0, 0);
-  fetch(min(kBKV, (ntiles - 1) * kBKV), 1);
-  stage(0, 0);
-  __syncthreads();
-  auto tile = [&](int t, int r) {        // r = t & 1 (a constant at each call site)
+  auto tile = [&](int t, int r) {        // r = (t - t_begin) & 1 (a constant at each call site)
     const int kv0 = t * kBKV;
-    fetch(min(kv0 + 2 * kBKV, (ntiles - 1) * kBKV), r);
+    fetch(min(kv0 + 2 * kBKV, last_kv), r);
     const char* Ks = lds + r * (KBUF + VBUF);
     const char* Vt = Ks + KBUF;
 
@@ -249,15 +262,33 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
     stage(r ^ 1, r ^ 1);
     __syncthreads();
   };
-  int t = 0;
-  for (; t + 1 < ntiles; t += 2) {
-    tile(t, 0);
-    tile(t + 1, 1);
+  if (t_begin < t_end) {                 // uniform over the workgroup
+    fetch(t_begin * kBKV, 0);
+    fetch(min((t_begin + 1) * kBKV, last_kv), 1);
+    stage(0, 0);
+    __syncthreads();
+    int t = t_begin;
+    for (; t + 1 < t_end; t += 2) {
+      tile(t, 0);
+      tile(t + 1, 1);
+    }
+    if (t < t_end) tile(t, 0);
   }
-  if (t < ntiles) tile(t, 0);
 
-  if (!q_ok) return;
   const float l_tot = l_run + __shfl_xor(l_run, 32);
+  if (!q_ok) return;
+  if constexpr (SPLIT) {
+    const size_t prow = ((size_t)sp * p.rows + (q_begin - p.qs.off[0] + qi)) * p.heads + head;
+    float* po = p.part_o + prow * HD;
+#pragma unroll
+    for (int h = 0; h < HT; ++h)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4)
+        *reinterpret_cast<float4*>(po + h * 32 + 8 * q4 + 4 * g) =
+            make_float4(oacc[h][4 * q4], oacc[h][4 * q4 + 1], oacc[h][4 * q4 + 2], oacc[h][4 * q4 + 3]);
+    if (g == 0) *reinterpret_cast<float2*>(p.part_ml + prow * 2) = make_float2(m_run * c, l_tot);
+    return;
+  }
   const float inv = 1.0f / l_tot;
   T* orow = reinterpret_cast<T*>(p.o + ((size_t)(q_begin + qi) * p.ldo + head * HD) * ES);
 #pragma unroll
@@ -279,8 +310,64 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
     }
 }
 
+// Merge of the key-range splits: one thread per (query row, head, 4 output
+// columns). With M = max_s m_s, w_s = 2^(m_s - M): o = sum_s w_s O_s / sum_s w_s l_s.
+template <typename T, int HD>
+__global__ __launch_bounds__(256) void k_attn_combine(AttnArgs p) {
+  constexpr int D4 = HD / 4;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)p.rows * p.heads * D4) return;
+  const int d = (int)(i % D4) * 4;
+  const int64_t rh = i / D4;                           // row * heads + head
+  const int head = (int)(rh % p.heads);
+  const int64_t row = rh / p.heads;
+  const size_t split_stride = (size_t)p.rows * p.heads;
+  float mx = -INFINITY;
+  for (int s = 0; s < p.splits; ++s) mx = fmaxf(mx, p.part_ml[(s * split_stride + rh) * 2]);
+  float l = 0.0f;
+  float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  for (int s = 0; s < p.splits; ++s) {
+    const float2 ml = *reinterpret_cast<const float2*>(p.part_ml + (s * split_stride + rh) * 2);
+    const float w = exp2f(ml.x - mx);                  // 0 for an empty split (max -inf)
+    const float4 o = *reinterpret_cast<const float4*>(p.part_o + (s * split_stride + rh) * HD + d);
+    l += w * ml.y;
+    acc.x += w * o.x;
+    acc.y += w * o.y;
+    acc.z += w * o.z;
+    acc.w += w * o.w;
+  }
+  const float inv = 1.0f / l;
+  T* dst = reinterpret_cast<T*>(p.o) + (size_t)(p.qs.off[0] + row) * p.ldo + head * HD + d;
+  if constexpr (sizeof(T) == 2) {
+    bf16x4 o4;
+    o4[0] = (bf16)(acc.x * inv);
+    o4[1] = (bf16)(acc.y * inv);
+    o4[2] = (bf16)(acc.z * inv);
+    o4[3] = (bf16)(acc.w * inv);
+    *reinterpret_cast<bf16x4*>(dst) = o4;
+  } else {
+    *reinterpret_cast<float4*>(dst) = make_float4(acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv);
+  }
+}
+
+template <typename T, int HD, int NW, int SITE>
+hipError_t launch_k(const AttnArgs& a, int tiles, hipStream_t s) {
+  const dim3 block(64 * NW);
+  if (a.splits == 1) {
+    hipLaunchKernelGGL((k_attn<T, HD, NW, SITE, false>), dim3(tiles * a.heads), block, 0, s, a);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL((k_attn<T, HD, NW, SITE, true>), dim3(tiles * a.heads * a.splits), block, 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t n = (int64_t)a.rows * a.heads * (HD / 4);
+  hipLaunchKernelGGL((k_attn_combine<T, HD>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+// splits > 1 requires a.part_o / a.part_ml sized for them.
 template <int NW, int SITE>
-hipError_t launch_a(int dt, int hd, const AttnArgs& a0, int heads, hipStream_t s) {
+hipError_t launch_a(int dt, int hd, const AttnArgs& a0, int heads, int splits, hipStream_t s) {
   AttnArgs a = a0;
   constexpr int BQ = 32 * NW;
   a.tile_off[0] = 0;
@@ -288,29 +375,51 @@ hipError_t launch_a(int dt, int hd, const AttnArgs& a0, int heads, hipStream_t s
   const int tiles = a.tile_off[a.qs.B];
   if (tiles == 0) return hipSuccess;
   a.heads = heads;
-  dim3 grid(tiles * heads), block(64 * NW);
-  if (dt == DT_BF16 && hd == 64) hipLaunchKernelGGL((k_attn<bf16, 64, NW, SITE>), grid, block, 0, s, a);
-  else if (dt == DT_BF16 && hd == 32) hipLaunchKernelGGL((k_attn<bf16, 32, NW, SITE>), grid, block, 0, s, a);
-  else if (dt == DT_F32 && hd == 64) hipLaunchKernelGGL((k_attn<float, 64, NW, SITE>), grid, block, 0, s, a);
-  else if (dt == DT_F32 && hd == 32) hipLaunchKernelGGL((k_attn<float, 32, NW, SITE>), grid, block, 0, s, a);
-  else return hipErrorInvalidValue;
-  return hipGetLastError();
+  a.splits = splits;
+  a.rows = a.qs.off[a.qs.B] - a.qs.off[0];
+  if (dt == DT_BF16 && hd == 64) return launch_k<bf16, 64, NW, SITE>(a, tiles, s);
+  if (dt == DT_BF16 && hd == 32) return launch_k<bf16, 32, NW, SITE>(a, tiles, s);
+  if (dt == DT_F32 && hd == 64) return launch_k<float, 64, NW, SITE>(a, tiles, s);
+  if (dt == DT_F32 && hd == 32) return launch_k<float, 32, NW, SITE>(a, tiles, s);
+  return hipErrorInvalidValue;
 }
 
-// 4 waves (128 queries) per workgroup when that still gives about two
-// workgroups per CU, else 2 waves (64 queries).
+// Bytes of split partials for `splits` splits of `rows` query rows.
+inline size_t split_bytes(int splits, int rows, int heads, int hd) {
+  return (size_t)splits * rows * heads * (hd + 2) * sizeof(float);
+}
+
+// 4 waves (128 queries) per workgroup (measured on MI355X from 300 to 4096
+// queries: ahead of 2 waves at every size from 820 up, level below). The key
+// range is split only while all workgroups still fit in one round on 256 CUs
+// and every split keeps at least 8 key tiles: below that the partial-result
+// traffic and the merge launch cost more than the added parallelism.
 template <int SITE>
-hipError_t launch_site(int dt, int hd, const AttnArgs& a, int heads, hipStream_t s) {
-  long t128 = 0;
-  for (int b = 0; b < a.qs.B; ++b) t128 += (a.qs.off[b + 1] - a.qs.off[b] + 127) / 128;
-  if (t128 * heads >= 480) return launch_a<4, SITE>(dt, hd, a, heads, s);
-  return launch_a<2, SITE>(dt, hd, a, heads, s);
+hipError_t launch_site(int dt, int hd, const AttnArgs& a, int heads, float* ws, size_t ws_bytes, hipStream_t s) {
+  long t128 = 0, kt_min = 1L << 30;
+  for (int b = 0; b < a.qs.B; ++b) {
+    const int nq = a.qs.off[b + 1] - a.qs.off[b];
+    if (nq == 0) continue;
+    t128 += (nq + 127) / 128;
+    kt_min = std::min<long>(kt_min, (a.ks.off[b + 1] - a.ks.off[b] + kBKV - 1) / kBKV);
+  }
+  int splits = 1;
+  while (splits < 8 && t128 * heads * splits * 2 <= 256 && kt_min >= 16 * splits) splits *= 2;
+  const int rows = a.qs.off[a.qs.B] - a.qs.off[0];
+  while (splits > 1 && (!ws || split_bytes(splits, rows, heads, hd) > ws_bytes)) splits /= 2;
+  AttnArgs b = a;
+  if (splits > 1) {
+    b.part_o = ws;
+    b.part_ml = ws + (size_t)splits * rows * heads * hd;
+  }
+  return launch_a<4, SITE>(dt, hd, b, heads, splits, s);
 }
 
 }  // namespace
 
 hipError_t launch_attention(int site, int dt, int heads, int hd, const Segs& qs, const Segs& ks, const void* q,
-                            int ldq, const void* k, int ldk, const void* v, int ldv, void* o, int ldo, hipStream_t s) {
+                            int ldq, const void* k, int ldk, const void* v, int ldv, void* o, int ldo, float* ws,
+                            size_t ws_bytes, hipStream_t s) {
   AttnArgs a;
   a.qs = qs;
   a.ks = ks;
@@ -323,9 +432,11 @@ hipError_t launch_attention(int site, int dt, int heads, int hd, const Segs& qs,
   a.ldv = ldv;
   a.ldo = ldo;
   a.scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
-  if (site == SITE_SELF) return launch_site<SITE_SELF>(dt, hd, a, heads, s);
-  if (site == SITE_CROSS) return launch_site<SITE_CROSS>(dt, hd, a, heads, s);
-  return launch_site<SITE_OP>(dt, hd, a, heads, s);
+  a.splits = 1;
+  a.part_o = a.part_ml = nullptr;
+  if (site == SITE_SELF) return launch_site<SITE_SELF>(dt, hd, a, heads, ws, ws_bytes, s);
+  if (site == SITE_CROSS) return launch_site<SITE_CROSS>(dt, hd, a, heads, ws, ws_bytes, s);
+  return launch_site<SITE_OP>(dt, hd, a, heads, ws, ws_bytes, s);
 }
 
 }  // namespace f3c

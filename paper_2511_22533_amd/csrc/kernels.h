@@ -76,7 +76,10 @@ hipError_t launch_gemm(int site, int dt, int epi, int M, int N, int K, const voi
 // Varlen multi-head softmax attention. Queries of sample b are rows
 // [qs.off[b], qs.off[b+1]) of q; its keys/values are rows [ks.off[b], ks.off[b+1])
 // of k and v. Head h uses columns [h*hd, (h+1)*hd). Output rows match queries.
+// ws (f32, ws_bytes, 16-byte aligned) may be null; when present, launches
+// with few query tiles split the key range and merge the splits through it.
 hipError_t launch_attention(int site, int dt, int heads, int hd, const Segs& qs, const Segs& ks, const void* q,
-                            int ldq, const void* k, int ldk, const void* v, int ldv, void* o, int ldo, hipStream_t s);
+                            int ldq, const void* k, int ldk, const void* v, int ldv, void* o, int ldo, float* ws,
+                            size_t ws_bytes, hipStream_t s);
 
 }  // namespace f3c

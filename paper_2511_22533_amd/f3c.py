@@ -72,7 +72,7 @@ _SIGS = {
     "f3c_op_gemm": (c_int, [c_int, c_int, c_int, c_int, c_int, c_p, c_int, c_p, c_int, c_p, c_p, c_p, c_int, c_p,
                             c_int, c_p, c_sz, c_p]),
     "f3c_op_attention": (c_int, [c_int, c_int, c_int, c_int, P_i32, P_i32, c_p, c_int, c_p, c_int, c_p, c_int, c_p,
-                                 c_int, c_p]),
+                                 c_int, c_p, c_sz, c_p]),
     "f3c_op_ln_mod": (c_int, [c_int, c_int, c_int, c_p, c_p, c_p, c_p, c_p]),
     "f3c_op_modulation": (c_int, [c_p, c_d, c_p, c_p, c_p]),
     "f3c_time_grid": (c_int, [c_int, c_d, P_d]),
@@ -342,11 +342,12 @@ def op_gemm(dtype: int, epilogue: int, A, W, bias, out=None, resid=None, gate=No
                             _stream(stream)))
 
 
-def op_attention(dtype: int, heads: int, head_dim: int, q_off, k_off, q, k, v, o, stream=None):
+def op_attention(dtype: int, heads: int, head_dim: int, q_off, k_off, q, k, v, o, workspace=None, stream=None):
     B = len(q_off) - 1
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     check(lib().f3c_op_attention(dtype, heads, head_dim, B, _i32(q_off), _i32(k_off), q.data_ptr(), q.stride(0),
                                  k.data_ptr(), k.stride(0), v.data_ptr(), v.stride(0), o.data_ptr(), o.stride(0),
-                                 _stream(stream)))
+                                 _ptr(workspace), ws_bytes, _stream(stream)))
 
 
 def op_ln_mod(dtype: int, h, out, shift=None, scale=None, stream=None):

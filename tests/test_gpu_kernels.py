@@ -156,7 +156,7 @@ def test_gemm_f32(torch, M, N, K, epi):
     assert max_rel(got, want) < 1e-5
 
 
-def _attn_case(torch, dt, heads, hd, q_lens, k_lens, seed, sample_queries=None):
+def _attn_case(torch, dt, heads, hd, q_lens, k_lens, seed, sample_queries=None, workspace=False, outputs=None):
     from paper_2511_22533_amd import f3c
     rng = np.random.default_rng(seed)
     d = heads * hd
@@ -169,11 +169,14 @@ def _attn_case(torch, dt, heads, hd, q_lens, k_lens, seed, sample_queries=None):
     if dt == f3c.F3C_BF16:
         q, k, v = bf16_round(q), bf16_round(k), bf16_round(v)
     o = torch.zeros((max(q_off[-1], 1), d), dtype=tdt, device="cuda")
-    say("attention", dt, heads, hd, list(q_lens), list(k_lens))
+    ws = torch.empty(8 << 20, dtype=torch.float32, device="cuda") if workspace else None
+    say("attention", dt, heads, hd, list(q_lens), list(k_lens), "workspace" if workspace else "")
     f3c.op_attention(dt, heads, hd, q_off.tolist(), k_off.tolist(), to_dev(q, tdt), to_dev(k, tdt),
-                     to_dev(v, tdt), o)
+                     to_dev(v, tdt), o, workspace=ws)
     torch.cuda.synchronize()
     got = o.float().cpu().numpy()
+    if outputs is not None:
+        outputs.append(got)
     worst = 0.0
     for b in range(len(q_lens)):
         if q_lens[b] == 0:
@@ -205,6 +208,28 @@ def test_self_attention_bf16_full_size_sampled(torch):
 def test_cross_attention_bf16(torch, q_lens):
     from paper_2511_22533_amd import f3c
     assert _attn_case(torch, f3c.F3C_BF16, 16, 64, q_lens, [1374] * len(q_lens), seed=len(q_lens)) < 2e-2
+
+
+# With a workspace, launches with few query tiles split the key range and
+# merge the partial results in a fixed order. Splits chosen for these cases:
+# 2, 2, 2, 2, 4, 8, and none for the last two.
+@pytest.mark.parametrize("q_lens,k_lens", [([1000], [1000]), ([820], [1374]), ([5, 300, 0, 77], [1374] * 4),
+                                           ([300], [1374]), ([1, 40], [4096, 2000]), ([64], [8192]),
+                                           ([1310], [1310]), ([820], [820])])
+def test_attention_bf16_split_keys(torch, q_lens, k_lens):
+    from paper_2511_22533_amd import f3c
+    outs = []
+    for rep in range(2):
+        assert _attn_case(torch, f3c.F3C_BF16, 16, 64, q_lens, k_lens, seed=sum(k_lens), workspace=True,
+                          outputs=outs) < 2e-2
+    assert np.array_equal(outs[0], outs[1])
+
+
+@pytest.mark.parametrize("hd,heads", [(32, 4), (64, 2)])
+def test_attention_f32_split_keys(torch, hd, heads):
+    from paper_2511_22533_amd import f3c
+    # 2 key splits
+    assert _attn_case(torch, f3c.F3C_F32, heads, hd, [512, 70], [2048, 1100], seed=hd, workspace=True) < 1e-4
 
 
 @pytest.mark.parametrize("hd,heads", [(32, 4), (64, 2)])
