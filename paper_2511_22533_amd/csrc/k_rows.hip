@@ -194,9 +194,11 @@ __global__ __launch_bounds__(256) void k_euler(float* __restrict__ x, const floa
 // y[r] = W[r] . f(x) + b[r] (optionally SiLU(y)). The input vector is staged in
 // LDS once per workgroup (optionally through SiLU, or generated as the
 // sinusoidal timestep features [cos(1000 t f_j), sin(1000 t f_j)],
-// f_j = 10000^(-j/half), evaluated in fp64); each wavefront then streams 16
-// weight rows with 16-byte loads.
-constexpr int kGemvRowsPerWave = 16;
+// f_j = 10000^(-j/half), evaluated in fp64); each wavefront then streams one
+// weight row with 16-byte loads. One row per wave: the 1024-row timestep MLP
+// then spans 256 workgroups instead of a few waves walking rows one after the
+// other at HBM latency each.
+constexpr int kGemvRowsPerWave = 1;
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_gemv(const T* __restrict__ W, const float* __restrict__ bias,
