@@ -98,19 +98,20 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
   // Tile staging: K row-major, V transposed (pairs of keys per 32/64-bit write).
   // Keys past the end are read from the last key (always valid) and masked.
   // Two register sets: tile t+2 is fetched while tile t+1 waits to be staged.
+  // Every thread issues the same loads (threads past the item count re-read
+  // the last item and skip the LDS write): a branch around some of the loads
+  // would make the compiler's wait before staging cover the loads in flight.
   u32x4 rk[2][KCH], rv[2][VPR][2];
   auto fetch = [&](int kv0, int r) {
 #pragma unroll
     for (int q = 0; q < KCH; ++q) {
-      const int ch = tid + NT * q, row = ch / CPR, col = ch % CPR;
-      if (KITEMS % NT != 0 && ch >= KITEMS) break;
+      const int ch = min(tid + NT * q, KITEMS - 1), row = ch / CPR, col = ch % CPR;
       const int key = min(kv0 + row, nk - 1);
       rk[r][q] = *reinterpret_cast<const u32x4*>(p.k + ((size_t)(k_begin + key) * p.ldk + head * HD) * ES + col * 16);
     }
 #pragma unroll
     for (int q = 0; q < VPR; ++q) {
-      const int it = tid + NT * q, pr = it / CPR, col = it % CPR;
-      if (VITEMS % NT != 0 && it >= VITEMS) break;
+      const int it = min(tid + NT * q, VITEMS - 1), pr = it / CPR, col = it % CPR;
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const int key = min(kv0 + 2 * pr + h, nk - 1);
@@ -389,20 +390,24 @@ inline size_t split_bytes(int splits, int rows, int heads, int hd) {
   return (size_t)splits * rows * heads * (hd + 2) * sizeof(float);
 }
 
-// 4 waves (128 queries) per workgroup (measured on MI355X from 300 to 4096
-// queries: ahead of 2 waves at every size from 820 up, level below). The key
-// range is split only while all workgroups still fit in one round on 256 CUs
-// and every split keeps at least 8 key tiles: below that the partial-result
-// traffic and the merge launch cost more than the added parallelism.
+// 8 waves (256 queries) per workgroup when that still gives at least 160
+// workgroups, else 4 waves (128 queries). Eight waves share each staged K/V
+// tile, which halves the staging work per query; measured on MI355X from 300
+// to 4096 queries, 8 waves lead from about 2300 queries up and 4 waves below.
+// The key range is split only while all workgroups still fit in one round on
+// 256 CUs and every split keeps at least 8 key tiles: below that the
+// partial-result traffic and the merge launch cost more than the parallelism.
 template <int SITE>
 hipError_t launch_site(int dt, int hd, const AttnArgs& a, int heads, float* ws, size_t ws_bytes, hipStream_t s) {
-  long t128 = 0, kt_min = 1L << 30;
+  long t128 = 0, t256 = 0, kt_min = 1L << 30;
   for (int b = 0; b < a.qs.B; ++b) {
     const int nq = a.qs.off[b + 1] - a.qs.off[b];
     if (nq == 0) continue;
     t128 += (nq + 127) / 128;
+    t256 += (nq + 255) / 256;
     kt_min = std::min<long>(kt_min, (a.ks.off[b + 1] - a.ks.off[b] + kBKV - 1) / kBKV);
   }
+  if (t256 * heads >= 160) return launch_a<8, SITE>(dt, hd, a, heads, 1, s);
   int splits = 1;
   while (splits < 8 && t128 * heads * splits * 2 <= 256 && kt_min >= 16 * splits) splits *= 2;
   const int rows = a.qs.off[a.qs.B] - a.qs.off[0];

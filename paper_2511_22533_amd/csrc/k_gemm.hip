@@ -187,16 +187,29 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs p) {
     __syncthreads();
     auto step = [&](int kt, int rr, int rl) {   // rr = kt % PF, rl = kt % 2 (constants below)
       load_tile(min(kt + PF, KT - 1), rr);
+      // 64 x 64 tiles: keep the loads ahead of the compute. Scheduled after it
+      // (to save registers) they leave nothing in flight when the older set is
+      // staged, so the staging waits for every outstanding load (measured on
+      // MI355X: fc2 at M = 820, 24.5 -> 20.9 us). The larger tiles are faster
+      // with the compiler's own interleaving.
+      if constexpr (BM == 64 && BN == 64) __builtin_amdgcn_sched_barrier(0);
       compute(rl);
       store_tile(rl ^ 1, rr + 1 == PF ? 0 : rr + 1);
       __syncthreads();
     };
+    // Whole groups of U steps in the loop and the remainder after it, so the
+    // loop's back edge is always taken after the last step of a group: the
+    // register sets then have the same pending loads on every entry to the
+    // loop head, and the compiler's waits there cover only the oldest group.
     constexpr int U = PF == 3 ? 6 : 2;
-    for (int kt = 0; kt < KT; kt += U) {
+    int kt = 0;
+    for (; kt + U <= KT; kt += U) {
 #pragma unroll
-      for (int i = 0; i < U; ++i)
-        if (kt + i < KT) step(kt + i, i % PF, i & 1);
+      for (int i = 0; i < U; ++i) step(kt + i, i % PF, i & 1);
     }
+#pragma unroll
+    for (int i = 0; i < U - 1; ++i)
+      if (kt + i < KT) step(kt + i, i % PF, i & 1);
   }
 
   // Epilogue. Tile (i, j), group q: activation row m0 + wm*BM/2 + 32 i + r32,

@@ -239,6 +239,12 @@ def test_attention_f32(torch, hd, heads, q_lens, k_lens):
     assert _attn_case(torch, f3c.F3C_F32, heads, hd, q_lens, k_lens, seed=hd + len(q_lens)) < 1e-4
 
 
+def test_attention_f32_eight_waves_sampled(torch):
+    # enough query tiles (21 x 8 heads) for the 8-wave workgroup
+    from paper_2511_22533_amd import f3c
+    assert _attn_case(torch, f3c.F3C_F32, 8, 64, [5200], [5200], seed=11, sample_queries=64) < 1e-4
+
+
 def test_attention_bf16_hd32(torch):
     from paper_2511_22533_amd import f3c
     assert _attn_case(torch, f3c.F3C_BF16, 4, 32, [300, 64], [300, 64], seed=9) < 2e-2
