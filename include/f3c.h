@@ -225,6 +225,37 @@ int f3c_op_ln_mod(int32_t dtype, int32_t rows, int32_t d, const float* h, const 
 int f3c_op_modulation(const f3c_model* m, double t, float* mod_dev, float* scratch_dev /* 2*width f32 */,
                       f3c_stream stream);
 
+/* Gather + embedding (Sec. 4.2: the transformer input is x at the active
+ * indices; Algorithm 1 FlowTransformer input). For sample b and its r-th
+ * active token i = idx_active[act_off[b] + r]:
+ *   h[act_off[b] + r][:] = x[b][i][:] W_in^T + b_in + P[i][:]
+ * with the model's input projection W_in, b_in and position table P.
+ * x f32 [B][N][8] (N = grid^3); idx_active int32 [act_off[B]] (NULL: every
+ * token active, identity order; then each segment must hold N rows);
+ * act_off_host: B+1 non-decreasing host ints from act_off[0] = 0, each
+ * segment 0..N rows; h f32 [act_off[B]][width]. Requires loaded weights
+ * (F3C_ESTATE otherwise). */
+int f3c_op_embed(const f3c_model* m, int32_t batch, const float* x, const int32_t* idx_active,
+                 const int32_t* act_off_host, float* h, f3c_stream stream);
+
+/* Final LayerNorm (no affine, eps 1e-6) and output projection (Algorithm 1
+ * FlowTransformer output): v_act f32 [rows][8] = LN(h) W_out^T + b_out,
+ * h f32 [rows][width]. Requires loaded weights. */
+int f3c_op_final(const f3c_model* m, int32_t rows, const float* h, float* v_act, f3c_stream stream);
+
+/* Merge, Euler update and cache rotation (Algorithm 1, update after the
+ * forward): for sample b and token i, v = pos[b][i] >= 0 ? v_act[pos[b][i]] :
+ * v_cache[b][i]; x[b][i] = x[b][i] - dt * v (product and difference each
+ * rounded to float32, no FMA) with dt = float32(t - t_next) computed in
+ * double; v_new[b][i] = v. x, v_cache, v_new f32 [B][n_tokens][8]; v_act f32
+ * [act_off[B]][8] (may be NULL when no token is active); pos int32
+ * [B][n_tokens] with packed rows act_off[b] + r or -1 (NULL: every token
+ * active at row act_off[b] + i). v_new must not alias v_cache (the step writes
+ * it over the dead v_prev). x is updated in place. */
+int f3c_op_euler(int32_t batch, int32_t n_tokens, float* x, const float* v_cache, const float* v_act,
+                 const int32_t* pos, const int32_t* act_off_host, double t, double t_next, float* v_new,
+                 f3c_stream stream);
+
 /* ----------------------------------------------------------- host schedules */
 
 /* Timestep grid t_k = shift(1 - (k-1)/T), k = 1..T+1 (Eq. S1 with factor eta;

@@ -753,6 +753,60 @@ int f3c_op_modulation(const f3c_model* m, double t, float* mod_dev, float* scrat
   return F3C_OK;
 }
 
+// Segment table from B+1 host offsets; each segment at most `cap` rows.
+static int segs_from_host(int32_t batch, const int32_t* off_host, int cap, Segs* out) {
+  if (batch < 1 || batch > F3C_MAX_BATCH) return fail(F3C_EINVAL, "batch must be in 1..%d", F3C_MAX_BATCH);
+  if (!off_host) return fail(F3C_EINVAL, "NULL offsets");
+  out->B = batch;
+  for (int b = 0; b <= batch; ++b) {
+    out->off[b] = off_host[b];
+    if (b == 0 && off_host[0] < 0) return fail(F3C_EINVAL, "negative offset");
+    if (b > 0 && (off_host[b] < off_host[b - 1] || off_host[b] - off_host[b - 1] > cap))
+      return fail(F3C_EINVAL, "segment %d must hold 0..%d rows", b - 1, cap);
+  }
+  return F3C_OK;
+}
+
+int f3c_op_embed(const f3c_model* m, int32_t batch, const float* x, const int32_t* idx_active,
+                 const int32_t* act_off_host, float* h, f3c_stream stream) {
+  if (!m || !x || !h) return fail(F3C_EINVAL, "NULL argument");
+  if (!m->loaded) return fail(F3C_ESTATE, "weights not loaded");
+  Segs act{};
+  if (int rc = segs_from_host(batch, act_off_host, m->N, &act)) return rc;
+  if (act.off[0] != 0) return fail(F3C_EINVAL, "act_off[0] must be 0");
+  if (!idx_active)
+    for (int b = 0; b < batch; ++b)
+      if (act.off[b + 1] - act.off[b] != m->N) return fail(F3C_EINVAL, "without idx_active every token is active");
+  HIP_TRY(launch_embed(m->cfg.dtype, x, m->N, idx_active, act, m->w("in_w"), m->b("in_b"), m->w("pos"), m->d, h,
+                       (hipStream_t)stream));
+  return F3C_OK;
+}
+
+int f3c_op_final(const f3c_model* m, int32_t rows, const float* h, float* v_act, f3c_stream stream) {
+  if (!m || !h || !v_act || rows < 0) return fail(F3C_EINVAL, "bad argument");
+  if (!m->loaded) return fail(F3C_ESTATE, "weights not loaded");
+  HIP_TRY(launch_final(m->cfg.dtype, h, rows, m->d, m->w("out_w"), m->b("out_b"), v_act, (hipStream_t)stream));
+  return F3C_OK;
+}
+
+int f3c_op_euler(int32_t batch, int32_t n_tokens, float* x, const float* v_cache, const float* v_act,
+                 const int32_t* pos, const int32_t* act_off_host, double t, double t_next, float* v_new,
+                 f3c_stream stream) {
+  if (!x || !v_cache || !v_new) return fail(F3C_EINVAL, "NULL argument");
+  if (n_tokens < 1) return fail(F3C_EINVAL, "n_tokens must be positive");
+  if (v_new == v_cache) return fail(F3C_EINVAL, "v_new must not alias v_cache");
+  if (!std::isfinite(t) || !std::isfinite(t_next)) return fail(F3C_EINVAL, "t and t_next must be finite");
+  Segs act{};
+  if (int rc = segs_from_host(batch, act_off_host, n_tokens, &act)) return rc;
+  if (act.off[batch] > act.off[0] && !v_act) return fail(F3C_EINVAL, "active rows need v_act");
+  if (!pos)
+    for (int b = 0; b < batch; ++b)
+      if (act.off[b + 1] - act.off[b] != n_tokens) return fail(F3C_EINVAL, "without pos every token is active");
+  const float dtf = (float)(t - t_next);
+  HIP_TRY(launch_euler(x, v_cache, v_act, pos, act, batch, n_tokens, dtf, v_new, (hipStream_t)stream));
+  return F3C_OK;
+}
+
 // ------------------------------------------------------------ host schedules
 
 static double shift_time(double u, double eta) { return eta * u / (1.0 + (eta - 1.0) * u); }

@@ -75,6 +75,9 @@ _SIGS = {
                                  c_int, c_p, c_sz, c_p]),
     "f3c_op_ln_mod": (c_int, [c_int, c_int, c_int, c_p, c_p, c_p, c_p, c_p]),
     "f3c_op_modulation": (c_int, [c_p, c_d, c_p, c_p, c_p]),
+    "f3c_op_embed": (c_int, [c_p, c_int, c_p, c_p, P_i32, c_p, c_p]),
+    "f3c_op_final": (c_int, [c_p, c_int, c_p, c_p, c_p]),
+    "f3c_op_euler": (c_int, [c_int, c_int, c_p, c_p, c_p, c_p, P_i32, c_d, c_d, c_p, c_p]),
     "f3c_time_grid": (c_int, [c_int, c_d, P_d]),
     "f3c_ceil_ratio": (c_int, [c_int, c_d]),
     "f3c_pcsc_quota": (c_int, [c_int, c_int, c_d, c_d, c_int, c_d]),
@@ -348,6 +351,22 @@ def op_attention(dtype: int, heads: int, head_dim: int, q_off, k_off, q, k, v, o
     check(lib().f3c_op_attention(dtype, heads, head_dim, B, _i32(q_off), _i32(k_off), q.data_ptr(), q.stride(0),
                                  k.data_ptr(), k.stride(0), v.data_ptr(), v.stride(0), o.data_ptr(), o.stride(0),
                                  _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def op_embed(model: "Model", x, act_off, h, idx_active=None, stream=None):
+    B = len(act_off) - 1
+    check(lib().f3c_op_embed(model.h, B, x.data_ptr(), _ptr(idx_active), _i32(act_off), h.data_ptr(),
+                             _stream(stream)))
+
+
+def op_final(model: "Model", h, v_act, stream=None):
+    check(lib().f3c_op_final(model.h, h.shape[0], h.data_ptr(), v_act.data_ptr(), _stream(stream)))
+
+
+def op_euler(x, v_cache, v_act, pos, act_off, t: float, t_next: float, v_new, stream=None):
+    B, N = x.shape[0], x.shape[1]
+    check(lib().f3c_op_euler(B, N, x.data_ptr(), v_cache.data_ptr(), _ptr(v_act), _ptr(pos), _i32(act_off),
+                             float(t), float(t_next), v_new.data_ptr(), _stream(stream)))
 
 
 def op_ln_mod(dtype: int, h, out, shift=None, scale=None, stream=None):

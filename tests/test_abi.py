@@ -98,6 +98,17 @@ def test_op_entry_validation_is_host_side(L):
     assert b"16-byte aligned" in L.f3c_last_error()
     assert L.f3c_op_ln_mod(1, 4, 96, 1, None, None, 1, None) == f3c.F3C_EINVAL
     assert b"unsupported d" in L.f3c_last_error()
+    m = f3c.Model(_cfg())                                   # no weights loaded
+    assert L.f3c_op_embed(m.h, 1, 1, None, f3c._i32([0, 512]), 1, None) == f3c.F3C_ESTATE
+    assert L.f3c_op_final(m.h, 4, 1, 1, None) == f3c.F3C_ESTATE
+    off = f3c._i32([0, 10, 20])
+    assert L.f3c_op_euler(2, 16, 1, 2, 3, 4, off, 1.0, 0.5, 2, None) == f3c.F3C_EINVAL     # v_new aliases v_cache
+    assert b"alias" in L.f3c_last_error()
+    assert L.f3c_op_euler(2, 16, 1, 2, 3, 4, off, math.inf, 0.5, 5, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_euler(2, 8, 1, 2, 3, 4, off, 1.0, 0.5, 5, None) == f3c.F3C_EINVAL     # segment > n_tokens
+    assert L.f3c_op_euler(2, 16, 1, 2, 3, None, off, 1.0, 0.5, 5, None) == f3c.F3C_EINVAL  # pos NULL, partial
+    assert L.f3c_op_euler(2, 16, 1, 2, None, 4, off, 1.0, 0.5, 5, None) == f3c.F3C_EINVAL  # rows but no v_act
+    assert L.f3c_op_euler(2, 16, 1, 2, 3, 4, f3c._i32([0, 10, 5]), 1.0, 0.5, 5, None) == f3c.F3C_EINVAL
 
 
 @pytest.mark.parametrize("steps,eta", [(10, 1.0), (25, 3.0), (25, 2.0), (50, 1.5)])

@@ -6,7 +6,9 @@
 * projections (MFMA GEMM, each epilogue) and attention (self, ragged varlen,
   cross with a non-tile-multiple key count) against float64 on the same
   bf16-rounded operands; bf16 bound 2e-2 max-rel, f32 bound 1e-4;
-* LayerNorm/modulation and the timestep modulation path.
+* LayerNorm/modulation and the timestep modulation path;
+* gather + embedding and the final LayerNorm + output projection against
+  float64; merge + Euler + cache rotation bit-exact against the oracle step.
 """
 import numpy as np
 import pytest
@@ -285,3 +287,103 @@ def test_modulation(torch, cfg):
         torch.cuda.synchronize()
         tol = 1e-4 if cfg.dtype == "f32" else 5e-3
         assert max_rel(got, om.modulation(t)) < tol
+
+
+_EMBED_CFGS = [synth.TINY, synth.ModelConfig(grid=16, width=1024, depth=1, heads=16, cond_tokens=8, cond_width=64,
+                                             dtype="bf16")]
+
+
+@pytest.mark.parametrize("cfg", _EMBED_CFGS, ids=["tiny_f32", "g16_w1024_bf16"])
+def test_embed_gather(torch, cfg):
+    from paper_2511_22533_amd import f3c
+    W = synth.make_weights(cfg, seed=4, scale=0.05)
+    m = f3c.Model(cfg).load(W)
+    om = dit.Model(cfg, W)
+    N, d = cfg.grid ** 3, cfg.width
+    rng = np.random.default_rng(17)
+    B = 3
+    x = rng.standard_normal((B, N, 8)).astype(np.float32)
+    # ragged active sets: a large one, a tiny one, an empty one (ascending indices)
+    sets = [np.sort(rng.choice(N, N - N // 5, replace=False)), np.array([0, N - 1]), np.zeros(0, np.int64)]
+    off = np.concatenate([[0], np.cumsum([len(a) for a in sets])]).astype(int)
+    idx = np.concatenate(sets).astype(np.int32)
+    h = torch.full((off[-1], d), float("nan"), dtype=torch.float32, device="cuda")
+    say("embed", cfg.dtype, off.tolist())
+    f3c.op_embed(m, to_dev(x), off.tolist(), h, idx_active=to_dev(idx))
+    torch.cuda.synchronize()
+    got = h.cpu().numpy()
+    for b in range(B):
+        if len(sets[b]):
+            want = om.embed(x[b][sets[b]], sets[b])
+            assert max_rel(got[off[b]:off[b + 1]], want) < 1e-5
+    # identity gather (full step): every token of each sample, no index list
+    h2 = torch.empty((2 * N, d), dtype=torch.float32, device="cuda")
+    say("embed identity", cfg.dtype)
+    f3c.op_embed(m, to_dev(x[:2]), [0, N, 2 * N], h2)
+    torch.cuda.synchronize()
+    got2 = h2.cpu().numpy()
+    for b in range(2):
+        assert max_rel(got2[b * N:(b + 1) * N], om.embed(x[b], np.arange(N))) < 1e-5
+
+
+@pytest.mark.parametrize("cfg", _EMBED_CFGS, ids=["tiny_f32", "g16_w1024_bf16"])
+@pytest.mark.parametrize("rows", [1, 333])
+def test_final_projection(torch, cfg, rows):
+    from paper_2511_22533_amd import f3c
+    W = synth.make_weights(cfg, seed=5, scale=0.05)
+    m = f3c.Model(cfg).load(W)
+    rng = np.random.default_rng(rows)
+    h = (2 * rng.standard_normal((rows, cfg.width)) + 0.5).astype(np.float32)
+    v = torch.full((rows, 8), float("nan"), dtype=torch.float32, device="cuda")
+    say("final", cfg.dtype, rows)
+    f3c.op_final(m, to_dev(h), v)
+    torch.cuda.synchronize()
+    want = dit.linear(dit.layer_norm(h.astype(np.float64)), W["out_w"], W["out_b"])
+    assert max_rel(v.cpu().numpy(), want) < 1e-5
+
+
+@pytest.mark.parametrize("N,n_cache", [(512, [0, 100, 512]), (4096, [3276, 0]), (32768, [22937])])
+def test_euler_merge_rotate_bit_exact(torch, N, n_cache):
+    """Merge + Euler + rotation equal the oracle's step bit for bit, with the
+    oracle's own selection and the same fresh velocities for the active rows."""
+    from oracle import sampler
+    from paper_2511_22533_amd import f3c
+    rng = np.random.default_rng(N)
+    B = len(n_cache)
+    x = rng.standard_normal((B, N, 8)).astype(np.float32)
+    vc = rng.standard_normal((B, N, 8)).astype(np.float32)
+    vp = rng.standard_normal((B, N, 8)).astype(np.float32)
+    sel = oracle_selection(vc, vp, n_cache)
+    act = [a for _, a in sel]
+    off = np.concatenate([[0], np.cumsum([len(a) for a in act])]).astype(int)
+    v_act = rng.standard_normal((max(off[-1], 1), 8)).astype(np.float32)
+    pos = np.full((B, N), -1, np.int32)
+    for b in range(B):
+        pos[b, act[b]] = off[b] + np.arange(len(act[b]))
+    t, t_next = 0.7310585786, 0.6224593312
+    st = sampler.State(x.copy(), vc.copy(), vp.copy())
+    sampler.step(st, lambda b, xa, idx, tt: v_act[off[b]:off[b + 1]], t, t_next, n_cache)
+    d_x, d_vn = to_dev(x), torch.full((B, N, 8), float("nan"), dtype=torch.float32, device="cuda")
+    say("euler", N, n_cache)
+    f3c.op_euler(d_x, to_dev(vc), to_dev(v_act), to_dev(pos), off.tolist(), t, t_next, d_vn)
+    torch.cuda.synchronize()
+    assert np.array_equal(d_x.cpu().numpy(), st.x)
+    assert np.array_equal(d_vn.cpu().numpy(), st.v_cache)
+
+
+def test_euler_all_active_without_pos(torch):
+    from oracle import sampler
+    from paper_2511_22533_amd import f3c
+    rng = np.random.default_rng(3)
+    B, N = 2, 512
+    x = rng.standard_normal((B, N, 8)).astype(np.float32)
+    vc = rng.standard_normal((B, N, 8)).astype(np.float32)
+    v_act = rng.standard_normal((B * N, 8)).astype(np.float32)
+    st = sampler.State(x.copy(), vc.copy(), vc.copy())
+    sampler.step(st, lambda b, xa, idx, tt: v_act[b * N:(b + 1) * N], 1.0, 0.96, [0, 0])
+    d_x, d_vn = to_dev(x), torch.empty((B, N, 8), dtype=torch.float32, device="cuda")
+    say("euler identity")
+    f3c.op_euler(d_x, to_dev(vc), to_dev(v_act), None, [0, N, 2 * N], 1.0, 0.96, d_vn)
+    torch.cuda.synchronize()
+    assert np.array_equal(d_x.cpu().numpy(), st.x)
+    assert np.array_equal(d_vn.cpu().numpy(), st.v_cache)
