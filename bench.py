@@ -50,7 +50,127 @@ def parse():
     ap.add_argument("--copy-ref-mb", type=int, default=0,
                     help="first run one plain device-to-device copy of this many MiB (a known-size reference "
                          "for hardware byte counters)")
+    ap.add_argument("--hbm-sweep", action="store_true",
+                    help="instead of the sampler: time the memory-bound kernels in isolation over a size sweep "
+                         "and report algorithmic bytes / kernel time against HBM peak")
     return ap.parse_args()
+
+
+def _event_time_ms(torch, fn, reps):
+    """Average duration of fn() over reps launches, HIP events on the current stream."""
+    fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        fn()
+    e1.record()
+    e1.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def _graph_time_ms(torch, fn, reps):
+    """Average kernel time of fn() with no host gaps: reps calls captured in
+    one HIP graph (the operator entries only enqueue kernels on the current
+    stream), replayed once to warm up, then timed over one replay."""
+    fn()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(reps):
+            fn()
+    graph.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    graph.replay()
+    e1.record()
+    e1.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def hbm_sweep():
+    """Isolated memory-bound kernels of the step through their C-ABI operator
+    entries. Algorithmic bytes per launch (what the kernel must move at least):
+      score+select  B*N*(64 + 4) + sum(n)*4   (two velocity caches in, pos + idx out)
+      embed         sum(n)*(32 + 2d + 4d)     (x row, bf16 position row, f32 h row)
+      merge+Euler   B*N*(32*4 + 4)            (x in/out, v in, v_new out, pos)
+      LN+mod        rows*d*(4 + 2)            (f32 h in, bf16 out)
+      modulation    the bf16 weights of the two timestep layers and all blocks' 6d outputs
+    Times are per launch with no host gaps (the launches of each size are
+    captured in one graph). The select kernel runs one workgroup per sample
+    (keys stay in LDS), so it cannot fill the chip below about 256 samples:
+    its figures are latency."""
+    import torch
+    from paper_2511_22533_amd import f3c, synth
+    torch.cuda.set_device(0)
+    g = torch.Generator(device="cuda").manual_seed(0)
+    rows_out = []
+
+    def add(kernel, shape, nbytes, ms):
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        rows_out.append({"kernel": kernel, "shape": shape, "bytes": int(nbytes), "us": round(ms * 1e3, 2),
+                         "GB/s": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4)})
+        print(f"[sweep] {kernel:12s} {shape:28s} {ms * 1e3:9.2f} us {gbs:8.1f} GB/s", file=sys.stderr, flush=True)
+
+    for B, N in [(1, 4096), (4, 4096), (16, 32768), (64, 32768)]:
+        vc = torch.randn((B, N, 8), device="cuda", generator=g)
+        vp = torch.randn((B, N, 8), device="cuda", generator=g)
+        n_cache = [int(0.8 * N)] * B
+        tot = sum(N - c for c in n_cache)
+        idx = torch.empty((tot,), dtype=torch.int32, device="cuda")
+        pos = torch.empty((B, N), dtype=torch.int32, device="cuda")
+        ms = _graph_time_ms(torch, lambda: f3c.op_select(vc, vp, 0.7, n_cache, idx, pos), 20)
+        add("select", f"B={B} N={N}", B * N * 68 + tot * 4, ms)
+        del vc, vp, idx, pos
+
+    cfg = synth.ModelConfig(grid=32, width=1024, depth=1, heads=16, cond_tokens=8, cond_width=64, dtype="bf16")
+    model = f3c.Model(cfg).load(synth.make_weights(cfg, seed=0))
+    N, d = cfg.grid ** 3, cfg.width
+    for B in (1, 4, 16):
+        x = torch.randn((B, N, 8), device="cuda", generator=g)
+        for frac in (0.3, 1.0):
+            n = int(frac * N)
+            idx = torch.sort(torch.randperm(N, device="cuda", generator=g)[:n])[0].to(torch.int32).repeat(B)
+            off = [b * n for b in range(B + 1)]
+            h = torch.empty((B * n, d), dtype=torch.float32, device="cuda")
+            ms = _graph_time_ms(torch, lambda: f3c.op_embed(model, x, off, h, idx_active=idx), 10)
+            add("embed", f"B={B} N={N} n={n}", B * n * (32 + 6 * d), ms)
+            del h
+        del x
+
+    for B, N in [(1, 4096), (16, 32768), (16, 1 << 20)]:
+        x = torch.randn((B, N, 8), device="cuda", generator=g)
+        vc = torch.randn((B, N, 8), device="cuda", generator=g)
+        vn = torch.empty_like(vc)
+        n = N // 5
+        va = torch.randn((B * n, 8), device="cuda", generator=g)
+        pos = torch.full((B, N), -1, dtype=torch.int32, device="cuda")
+        pos[:, :n] = torch.arange(B * n, device="cuda", dtype=torch.int32).view(B, n)
+        off = [b * n for b in range(B + 1)]
+        ms = _graph_time_ms(torch, lambda: f3c.op_euler(x, vc, va, pos, off, 0.5, 0.45, vn), 20)
+        add("euler", f"B={B} N={N}", B * N * 132, ms)
+        del x, vc, vn, va, pos
+
+    for rows in (820, 4096, 32768, 262144):
+        h = torch.randn((rows, 1024), device="cuda", generator=g)
+        out = torch.empty((rows, 1024), dtype=torch.bfloat16, device="cuda")
+        sh = torch.randn((1024,), device="cuda", generator=g)
+        sc = torch.randn((1024,), device="cuda", generator=g)
+        ms = _graph_time_ms(torch, lambda: f3c.op_ln_mod(f3c.F3C_BF16, h, out, sh, sc), 20)
+        add("ln_mod", f"rows={rows} d=1024", rows * 1024 * 6, ms)
+        del h, out
+
+    mcfg = synth.TRELLIS16
+    mm = f3c.Model(mcfg).load(synth.make_weights(mcfg, seed=0))
+    d, L = mcfg.width, mcfg.depth
+    mod = torch.empty((L * 6 * d,), dtype=torch.float32, device="cuda")
+    scratch = torch.empty((2 * d,), dtype=torch.float32, device="cuda")
+    ms = _graph_time_ms(torch, lambda: f3c.check(f3c.lib().f3c_op_modulation(
+        mm.h, 0.5, mod.data_ptr(), scratch.data_ptr(), f3c._stream(None))), 20)
+    wbytes = 2 * (256 * d + d * d + L * 6 * d * d) + 4 * L * 6 * d
+    add("modulation", f"L={L} d={d}", wbytes, ms)
+    print(json.dumps({"mode": "hbm_sweep", "peak_GB/s": PEAK_HBM_GBS, "rows": rows_out}), flush=True)
 
 
 def cpu_baseline(w, W, cond, x_T, quotas, times, depth):
@@ -111,6 +231,9 @@ def main():
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
                           "n_gpus": args.gpus}))
         sys.exit(2)
+    if args.hbm_sweep:
+        hbm_sweep()
+        return
 
     import torch
     from paper_2511_22533_amd import f3c, synth
@@ -189,6 +312,18 @@ def main():
     state.profile(False)
     print(f"[bench] timed {args.steps} steps in {elapsed * 1e3:.1f} ms", file=sys.stderr, flush=True)
 
+    # Full and cached steps timed apart (untimed for `value`): repeated full
+    # steps from a trajectory start, and repeated cached steps at the
+    # schedule's largest quota (its smallest active set).
+    state.reset()
+    x.copy_(x_T_dev)
+    state.set_cond(cond_dev)
+    full_ms = _event_time_ms(torch, lambda: state.full_step(x, float(times[0]), float(times[1])), 10)
+    k_min = int(np.argmax(quotas.sum(axis=1)))
+    q_min = quotas[k_min].tolist()
+    cached_ms = _event_time_ms(torch, lambda: state.cached_step(x, float(times[k_min]), float(times[k_min + 1]),
+                                                                q_min), 20) if any(q_min) else None
+
     peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
     achieved = prof["flops"] / (prof["ms"] * 1e-3) / 1e12 if prof["ms"] > 0 else 0.0
     roofline = {
@@ -221,6 +356,10 @@ def main():
                    "depth": cfg.depth, "heads": cfg.heads, "cond_tokens": cfg.cond_tokens, "batch": w.batch,
                    "steps_per_trajectory": T, "quota": w.schedule, "parallelism": "single GPU"},
         "active_tokens_per_s": round(active / elapsed, 1),
+        "samples_per_s": round(w.batch * args.steps / elapsed / T, 3),
+        "full_step_ms": round(full_ms, 4),
+        "cached_step_ms": round(cached_ms, 4) if cached_ms is not None else None,
+        "cached_step_active_tokens": int(sum(cfg.tokens - c for c in q_min)),
         "step_model_tflops": round(step_tflops, 2),
         "step_mfma_frac": round(step_tflops / peak, 4),
         "roofline": roofline,
