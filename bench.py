@@ -56,6 +56,36 @@ def parse():
     return ap.parse_args()
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "trellis16_cached_traffic.md")
+TRAFFIC_WORKLOAD = "trellis16_cached"
+
+
+def counter_traffic(cls: str, workload: str):
+    """HBM-side bytes per call of a kernel class from the committed FETCH_SIZE /
+    WRITE_SIZE counter summary of the trellis16_cached trajectory, or (None,
+    reason). The figure is used only while the SHA-256 of the kernel's source
+    files equals the one recorded with the counters."""
+    import hashlib
+    import re
+    if workload != TRAFFIC_WORKLOAD:
+        return None, f"counters were taken on {TRAFFIC_WORKLOAD} only"
+    if not os.path.exists(TRAFFIC_FILE):
+        return None, "no counter summary"
+    pat = re.compile(r"traffic (\w+): (\d+) bytes per call; sources (\S+) sha256 ([0-9a-f]{64})")
+    for line in open(TRAFFIC_FILE):
+        m = pat.search(line)
+        if not m or m.group(1) != cls:
+            continue
+        h = hashlib.sha256()
+        for name in m.group(3).split("+"):
+            with open(os.path.join(ROOT, "paper_2511_22533_amd", "csrc", name), "rb") as fh:
+                h.update(fh.read())
+        if h.hexdigest() != m.group(4):
+            return None, "kernel sources changed since the counters were taken"
+        return int(m.group(2)), "rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by a 256 MiB copy reference"
+    return None, f"no counter line for {cls}"
+
+
 def _event_time_ms(torch, fn, reps):
     """Average duration of fn() over reps launches, HIP events on the current stream."""
     fn()
@@ -326,6 +356,7 @@ def main():
 
     peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
     achieved = prof["flops"] / (prof["ms"] * 1e-3) / 1e12 if prof["ms"] > 0 else 0.0
+    traffic, traffic_src = counter_traffic(dominant, w.name)
     roofline = {
         "bound": "mfma",
         "kernel": dominant,
@@ -333,7 +364,9 @@ def main():
         "peak": peak,
         "unit": "TFLOP/s",
         "frac": round(achieved / peak, 4),
-        "traffic": None,
+        "traffic": traffic,
+        "traffic_source": traffic_src,
+        "algorithmic_bytes_per_launch": round(prof["bytes"] / max(prof["launches"], 1)),
         "launches": prof["launches"],
         "avg_launch_us": round(prof["ms"] * 1e3 / max(prof["launches"], 1), 2),
         "flops_per_launch": prof["flops"] / max(prof["launches"], 1),

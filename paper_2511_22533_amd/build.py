@@ -1,4 +1,5 @@
-"""Compile the gfx950 kernels and the C-ABI host library into lib/libf3c.so.
+"""Compile the gfx950 kernels and the C-ABI host library into lib/libf3c.so,
+and the torch-free command-line driver lib/f3c_drive linked against it.
 
 Every HIP source is compiled with hipcc for gfx950 only. Packed-FP32 VALU
 instructions are disabled and floating-point contraction is off (the scoring and
@@ -17,9 +18,11 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB_DIR = os.path.join(HERE, "lib")
 LIB = os.path.join(LIB_DIR, "libf3c.so")
+DRIVER = os.path.join(LIB_DIR, "f3c_drive")
 ROOT = os.path.dirname(HERE)
 
 SOURCES = ["k_select.hip", "k_rows.hip", "k_gemm.hip", "k_attn.hip", "f3c.cpp"]
+DRIVER_SOURCE = "f3c_drive.hip"
 
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-ffp-contract=off",
@@ -55,17 +58,24 @@ def _compile(src: str, obj: str) -> None:
 def build(verbose: bool = False) -> str:
     obj_dir = os.path.join(LIB_DIR, "obj")
     os.makedirs(obj_dir, exist_ok=True)
-    objs = [os.path.join(obj_dir, s.rsplit(".", 1)[0] + ".o") for s in SOURCES]
-    with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
-        list(ex.map(_compile, SOURCES, objs))
+    srcs = SOURCES + [DRIVER_SOURCE]
+    objs = [os.path.join(obj_dir, s.rsplit(".", 1)[0] + ".o") for s in srcs]
+    with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+        list(ex.map(_compile, srcs, objs))
     tmp = LIB + ".tmp"
-    cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs]
+    cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs[:-1]]
     r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed:\n" + r.stdout)
     os.replace(tmp, LIB)
+    tmp = DRIVER + ".tmp"
+    cmd = [hipcc(), "--offload-arch=gfx950", "-o", tmp, objs[-1], "-L" + LIB_DIR, "-lf3c", "-Wl,-rpath,$ORIGIN"]
+    r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("driver link failed:\n" + r.stdout)
+    os.replace(tmp, DRIVER)
     if verbose:
-        print("built", LIB)
+        print("built", LIB, "and", DRIVER)
     return LIB
 
 

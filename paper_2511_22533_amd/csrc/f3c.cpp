@@ -219,6 +219,13 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
     }
     const int dm = m->dm;
     const double lnb = rows * (double)d * (4 + es);
+    // Algorithmic bytes of the dense kernels (least data each must move):
+    // projections read A and W and write the output (f32 residual read and
+    // written); attention reads Q, K, V and writes O.
+    const double r = rows, dd = d, E = (double)es;
+    auto proj_bytes = [&](double n, double k, bool resid) { return (r * k + n * k) * E + r * n * (resid ? 8.0 : E); };
+    double cond_rows = 0;
+    for (int b = 0; b < B; ++b) cond_rows += (act.off[b + 1] > act.off[b]) ? m->Nc : 0;
     for (int l = 0; l < L; ++l) {
       const std::string p = "blk" + std::to_string(l) + ".";
       const float* md = s->mod + (size_t)l * 6 * d;
@@ -227,20 +234,20 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
         HIP_TRY(launch_ln_mod(dt, s->h, rows, d, md, md + d, s->u, st));
       }
       {
-        Scope sc(s, F3C_PROF_GEMM_QKV, st, 2.0 * rows * 3 * d * d, 0);
+        Scope sc(s, F3C_PROF_GEMM_QKV, st, 2.0 * rows * 3 * d * d, proj_bytes(3 * dd, dd, false));
         HIP_TRY(launch_gemm(SITE_QKV, dt, EPI_STORE, rows, 3 * d, d, s->u, d, m->w(p + "qkv_w"), d, m->b(p + "qkv_b"),
                             nullptr, s->qkv, 3 * d, nullptr, 0, s->ws, s->ws_bytes, st));
       }
       {
         double fl = 0;
         for (int b = 0; b < B; ++b) fl += 4.0 * (double)(act.off[b + 1] - act.off[b]) * (act.off[b + 1] - act.off[b]) * d;
-        Scope sc(s, F3C_PROF_ATTN_SELF, st, fl, 0);
+        Scope sc(s, F3C_PROF_ATTN_SELF, st, fl, 4.0 * r * dd * E);
         const char* q = static_cast<const char*>(s->qkv);
         HIP_TRY(launch_attention(SITE_SELF, dt, m->cfg.heads, m->hd, act, act, q, 3 * d, q + d * es, 3 * d, q + 2 * d * es,
                                  3 * d, s->att, d, s->ws, s->ws_bytes, st));
       }
       {
-        Scope sc(s, F3C_PROF_GEMM_O, st, 2.0 * rows * d * d, 0);
+        Scope sc(s, F3C_PROF_GEMM_O, st, 2.0 * rows * d * d, proj_bytes(dd, dd, true));
         HIP_TRY(launch_gemm(SITE_O, dt, EPI_RESID, rows, d, d, s->att, d, m->w(p + "o_w"), d, m->b(p + "o_b"), md + 2 * d,
                             nullptr, 0, s->h, d, s->ws, s->ws_bytes, st));
       }
@@ -249,18 +256,18 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
         HIP_TRY(launch_ln_mod(dt, s->h, rows, d, nullptr, nullptr, s->u, st));
       }
       {
-        Scope sc(s, F3C_PROF_GEMM_Q, st, 2.0 * rows * d * d, 0);
+        Scope sc(s, F3C_PROF_GEMM_Q, st, 2.0 * rows * d * d, proj_bytes(dd, dd, false));
         HIP_TRY(launch_gemm(SITE_Q, dt, EPI_STORE, rows, d, d, s->u, d, m->w(p + "q_w"), d, m->b(p + "q_b"), nullptr,
                             s->qc, d, nullptr, 0, s->ws, s->ws_bytes, st));
       }
       {
-        Scope sc(s, F3C_PROF_ATTN_CROSS, st, 4.0 * rows * m->Nc * d, 0);
+        Scope sc(s, F3C_PROF_ATTN_CROSS, st, 4.0 * rows * m->Nc * d, (2.0 * r + 2.0 * cond_rows) * dd * E);
         const char* kv = static_cast<const char*>(s->kv) + (size_t)l * 2 * d * es;
         HIP_TRY(launch_attention(SITE_CROSS, dt, m->cfg.heads, m->hd, act, cond_segs, s->qc, d, kv, 2 * L * d, kv + d * es,
                                  2 * L * d, s->att, d, s->ws, s->ws_bytes, st));
       }
       {
-        Scope sc(s, F3C_PROF_GEMM_CO, st, 2.0 * rows * d * d, 0);
+        Scope sc(s, F3C_PROF_GEMM_CO, st, 2.0 * rows * d * d, proj_bytes(dd, dd, true));
         HIP_TRY(launch_gemm(SITE_CO, dt, EPI_RESID, rows, d, d, s->att, d, m->w(p + "co_w"), d, m->b(p + "co_b"), nullptr,
                             nullptr, 0, s->h, d, s->ws, s->ws_bytes, st));
       }
@@ -269,12 +276,12 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
         HIP_TRY(launch_ln_mod(dt, s->h, rows, d, md + 3 * d, md + 4 * d, s->u, st));
       }
       {
-        Scope sc(s, F3C_PROF_GEMM_FC1, st, 2.0 * rows * dm * d, 0);
+        Scope sc(s, F3C_PROF_GEMM_FC1, st, 2.0 * rows * dm * d, proj_bytes(dm, dd, false));
         HIP_TRY(launch_gemm(SITE_FC1, dt, EPI_GELU, rows, dm, d, s->u, d, m->w(p + "fc1_w"), d, m->b(p + "fc1_b"), nullptr,
                             s->hid, dm, nullptr, 0, s->ws, s->ws_bytes, st));
       }
       {
-        Scope sc(s, F3C_PROF_GEMM_FC2, st, 2.0 * rows * d * dm, 0);
+        Scope sc(s, F3C_PROF_GEMM_FC2, st, 2.0 * rows * d * dm, proj_bytes(dd, dm, true));
         HIP_TRY(launch_gemm(SITE_FC2, dt, EPI_RESID, rows, d, dm, s->hid, dm, m->w(p + "fc2_w"), dm, m->b(p + "fc2_b"),
                             md + 5 * d, nullptr, 0, s->h, d, s->ws, s->ws_bytes, st));
       }
