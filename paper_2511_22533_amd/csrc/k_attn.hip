@@ -23,6 +23,7 @@
 // output with its reference max and sum in f32, and a second kernel merges the
 // splits in split order (the standard log-sum-exp combination; deterministic).
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -32,6 +33,33 @@ namespace f3c {
 namespace {
 
 constexpr int kBKV = 64;             // keys per LDS tile
+
+// 16 bytes per lane from global memory straight into LDS at lds_block + 16 *
+// lane (gfx950 global_load_lds_dwordx4; the block base is wave-uniform and
+// goes through M0). Written as inline assembly so that the compiler does not
+// track it: it would otherwise wait for every outstanding LDS load of this
+// kind before any LDS transpose read. The kernel orders these loads itself
+// (an s_waitcnt on the vector-memory counter and a barrier before a tile is
+// read); waits the compiler places for its own loads only grow more
+// conservative, since the counter retires in issue order.
+__device__ __forceinline__ void dma16(const char* gptr, char* lds_block) {
+  const uint32_t base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_block;
+  asm volatile("global_load_lds_dwordx4 %0, off" : : "v"(gptr), "{m0}"(__builtin_amdgcn_readfirstlane(base))
+               : "memory");
+}
+
+// max(a, b, c) as one v_max3_f32. fmaxf on MFMA results costs three
+// instructions each (both inputs are first quieted with v_max x, x, since the
+// compiler cannot prove they are not signalling NaNs); the scores here are
+// finite or -inf, never NaN.
+__device__ __forceinline__ float max3(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 constexpr float kRescaleLog2 = 8.0f;
 
 struct AttnArgs {
@@ -56,8 +84,16 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
   constexpr int BQ = 32 * NW;
   constexpr int ES = sizeof(T);
   constexpr int E = Mfma<T>::E;
-  constexpr int KRS = HD * ES + 16;          // K tile row stride (bytes)
-  constexpr int VRS = kBKV * ES + 8;         // V^T tile row stride (bytes)
+  // bf16 with 64-wide heads: K and V tiles go global -> LDS directly (16-byte
+  // DMA loads, no registers) into three buffers, row-major with 128-byte rows
+  // whose 16-byte chunks are XOR-swizzled by row (conflict-free fragment
+  // reads); V^T fragments come from the row-major V tile through the LDS
+  // transpose read. Other types and head sizes stage through registers, with
+  // V transposed on its way into LDS.
+  constexpr bool DMA = ES == 2 && HD == 64;
+  constexpr int NBUF = DMA ? 4 : 2;
+  constexpr int KRS = DMA ? HD * ES : HD * ES + 16;   // K tile row stride (bytes)
+  constexpr int VRS = kBKV * ES + 8;                 // V^T tile row stride (bytes), register path
   constexpr int NKS = HD * ES / 32;          // 32-byte K slices over the head dim
   constexpr int PER16 = 16 / ES;
   constexpr int MMA_PER_READ = PER16 / E;
@@ -67,8 +103,8 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
   constexpr int VITEMS = kBKV / 2 * CPR;    // V (key pair, chunk) items per tile
   constexpr int KCH = (KITEMS + NT - 1) / NT;
   constexpr int VPR = (VITEMS + NT - 1) / NT;
-  constexpr int KBUF = kBKV * KRS, VBUF = HD * VRS;
-  __shared__ __attribute__((aligned(16))) char lds[2 * (KBUF + VBUF)];
+  constexpr int KBUF = kBKV * KRS, VBUF = DMA ? kBKV * HD * ES : HD * VRS;
+  __shared__ __attribute__((aligned(16))) char lds[NBUF * (KBUF + VBUF)];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 5, r32 = lane & 31;
@@ -147,6 +183,35 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
     }
   };
 
+  // DMA path: one wave instruction fills 1 KiB = 8 rows; lane l writes 16-byte
+  // slot l, i.e. row l/8 and physical chunk l%8, with the logical chunk the
+  // row's swizzle maps there (XOR is its own inverse).
+  //   K: physical chunk = chunk ^ ((row >> 1) & 7)  (16 lanes read 16 rows)
+  //   V: physical chunk = chunk ^ (((row >> 1) & 1) << 2)  (transpose reads
+  //      take 32 bytes from each of 4 consecutive rows)
+  constexpr int DBLK = kBKV / 8;                       // 8-row blocks per tile
+  constexpr int DQ = (DBLK + NW - 1) / NW;             // blocks per wave
+  auto fetch_dma = [&](int kv0, int buf) {
+    char* Ks = lds + buf * (KBUF + VBUF);
+    char* Vs = Ks + KBUF;
+#pragma unroll
+    for (int q = 0; q < DQ; ++q) {
+      const int blk = min(wave + NW * q, DBLK - 1);
+      const int row = blk * 8 + (lane >> 3), phys = lane & 7;
+      const int key = min(kv0 + row, nk - 1);
+      const size_t kofs = ((size_t)(k_begin + key) * p.ldk + head * HD) * ES;
+      const size_t vofs = ((size_t)(k_begin + key) * p.ldv + head * HD) * ES;
+      dma16(p.k + kofs + ((phys ^ ((row >> 1) & 7)) << 4), Ks + blk * 1024);
+      dma16(p.v + vofs + ((phys ^ (((row >> 1) & 1) << 2)) << 4), Vs + blk * 1024);
+    }
+  };
+  // Wait until at most n vector-memory operations are outstanding (gfx9
+  // s_waitcnt encoding; expcnt and lgkmcnt left at their maxima).
+  auto wait_vm = [](auto n) {
+    constexpr int v = decltype(n)::value;
+    __builtin_amdgcn_s_waitcnt((v & 15) | (7 << 4) | (15 << 8) | ((v >> 4) << 14));
+  };
+
   f32x16 oacc[HT];
 #pragma unroll
   for (int t = 0; t < HT; ++t)
@@ -160,21 +225,23 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
   const int t_begin = sp * ntiles / nsp, t_end = (sp + 1) * ntiles / nsp;
   const int last_kv = (t_end - 1) * kBKV;
 
-  // Fetches are unconditional (past the end they re-read the last tile), so the
-  // wait before staging tile t+1 does not cover the loads of tile t+2.
-  auto tile = [&](int t, int r) {        // r = (t - t_begin) & 1 (a constant at each call site)
-    const int kv0 = t * kBKV;
-    fetch(min(kv0 + 2 * kBKV, last_kv), r);
-    const char* Ks = lds + r * (KBUF + VBUF);
-    const char* Vt = Ks + KBUF;
+  // Per-lane constants of the DMA path's fragment reads: the K swizzle of rows
+  // 32*kt + r32, and for the transpose read the source row and column within
+  // the lane's 16-lane group (rows kb + vi/4, columns db + 4*(vi%4)).
+  const int kswz = (r32 >> 1) & 7;
+  const int vi = lane & 15;
+  const int vrow = vi >> 2, vswz = ((vi >> 3) & 1) << 2, vcol = 4 * (vi & 3) + 16 * ((lane >> 4) & 1);
 
-    // S^T tiles: rows = keys kv0 + 32*kt + ..., cols = this wave's 32 queries.
-    f32x16 sacc[2];
+  // S^T tiles of the tile in buffer buf: rows = keys 32*kt + ..., cols = this
+  // wave's 32 queries.
+  auto qk = [&](int buf, f32x16 (&sacc)[2]) {
+    const char* Ks = lds + buf * (KBUF + VBUF);
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
 #pragma unroll
       for (int s = 0; s < NKS; ++s) {
-        const u32x4 kf = *reinterpret_cast<const u32x4*>(Ks + (kt * 32 + r32) * KRS + s * 32 + g * 16);
+        const u32x4 kf = DMA ? *reinterpret_cast<const u32x4*>(Ks + (kt * 32 + r32) * KRS + (((2 * s + g) ^ kswz) << 4))
+                             : *reinterpret_cast<const u32x4*>(Ks + (kt * 32 + r32) * KRS + s * 32 + g * 16);
 #pragma unroll
         for (int u = 0; u < MMA_PER_READ; ++u) {
           typename Mfma<T>::frag a, bq;
@@ -190,6 +257,12 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
         }
       }
     }
+  };
+
+  // Online softmax of tile t's scores and O^T += V^T P^T with V from buffer buf.
+  auto softmax_pv = [&](int t, int buf, f32x16 (&sacc)[2]) {
+    const int kv0 = t * kBKV;
+    const char* Vt = lds + buf * (KBUF + VBUF) + KBUF;
 
     // Key of element e: kv0 + 32*kt + 8*(e/4) + 4*g + e%4. Mask the ragged tail.
     if (kv0 + kBKV > nk) {
@@ -199,11 +272,14 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
         for (int e = 0; e < 16; ++e)
           if (kv0 + kt * 32 + 8 * (e >> 2) + 4 * g + (e & 3) >= nk) sacc[kt][e] = -INFINITY;
     }
-    float mx = fmaxf(sacc[0][0], sacc[0][1]);
+    // Max over this lane's 32 scores: two independent chains of v_max3.
+    float ma = max3(sacc[0][0], sacc[0][1], sacc[0][2]), mb = max3(sacc[1][0], sacc[1][1], sacc[1][2]);
 #pragma unroll
-    for (int e = 2; e < 16; e += 2) mx = fmaxf(mx, fmaxf(sacc[0][e], sacc[0][e + 1]));
-#pragma unroll
-    for (int e = 0; e < 16; e += 2) mx = fmaxf(mx, fmaxf(sacc[1][e], sacc[1][e + 1]));
+    for (int e = 3; e < 15; e += 2) {
+      ma = max3(ma, sacc[0][e], sacc[0][e + 1]);
+      mb = max3(mb, sacc[1][e], sacc[1][e + 1]);
+    }
+    float mx = max3(ma, mb, max3(sacc[0][15], sacc[1][15], -INFINITY));
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     // Lazy rescale: move the reference max only when it grows by more than 2^8.
     if (__builtin_amdgcn_ballot_w64((mx - m_run) * c > kRescaleLog2) != 0) {
@@ -246,34 +322,92 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
         }
 #pragma unroll
         for (int h = 0; h < HT; ++h) {
-          const char* vrow = Vt + (h * 32 + r32) * VRS;
           typename Mfma<T>::frag vf;
-          if constexpr (ES == 2) {
+          if constexpr (DMA) {
+            // keys kb..kb+3 and kb+8..kb+11 at column h*32 + (lane%32) through two
+            // transpose reads of the row-major V tile (K-slot order of P).
+            const int kb = kt * 32 + 16 * u + 4 * g, col = h * 32 + vcol;
+            const char* a0 = Vt + (kb + vrow) * (HD * ES) + ((((col >> 3) ^ vswz)) << 4) + (col & 7) * ES;
+            const auto lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)a0);
+            const auto hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(a0 + 8 * HD * ES));
+            vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+          } else if constexpr (ES == 2) {
+            const char* vrow = Vt + (h * 32 + r32) * VRS;
             const int key0 = kt * 32 + 16 * u + 4 * g;
             const u32x2 lo = *reinterpret_cast<const u32x2*>(vrow + key0 * ES);
             const u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + (key0 + 8) * ES);
             vf = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
           } else {
+            const char* vrow = Vt + (h * 32 + r32) * VRS;
             const int key = kt * 32 + 8 * (u >> 2) + 4 * g + (u & 3);
             vf = *reinterpret_cast<const float*>(vrow + key * ES);
           }
           oacc[h] = Mfma<T>::mma(vf, pf, oacc[h]);
         }
       }
-    stage(r ^ 1, r ^ 1);
-    __syncthreads();
   };
-  if (t_begin < t_end) {                 // uniform over the workgroup
-    fetch(t_begin * kBKV, 0);
-    fetch(min((t_begin + 1) * kBKV, last_kv), 1);
-    stage(0, 0);
-    __syncthreads();
-    int t = t_begin;
-    for (; t + 1 < t_end; t += 2) {
-      tile(t, 0);
-      tile(t + 1, 1);
+  auto compute = [&](int t, int buf) {
+    f32x16 sacc[2];
+    qk(buf, sacc);
+    softmax_pv(t, buf, sacc);
+  };
+
+  if constexpr (DMA) {
+    // Four buffers, tile t in buffer (t - t_begin) % 4, loads three tiles
+    // ahead. Step t waits for tile t + 1 (tile t + 2 stays in flight); the
+    // barrier makes every wave's DMA visible and retires buffer (t - 1) % 4,
+    // which receives tile t + 3 (clamped: past the end the last tile is
+    // re-read). Then the scores of tile t + 1 are issued to the matrix cores
+    // before the softmax of tile t, so that VALU work overlaps them.
+    if (t_begin < t_end) {               // uniform over the workgroup
+      // Q first: otherwise the compiler, which does not see the DMA, keeps its
+      // wait for the Q fragments inside the loop as a full vmcnt(0).
+      __builtin_amdgcn_sched_barrier(0);
+      wait_vm(std::integral_constant<int, 0>{});
+      fetch_dma(t_begin * kBKV, 0);
+      fetch_dma(min((t_begin + 1) * kBKV, last_kv), 1);
+      fetch_dma(min((t_begin + 2) * kBKV, last_kv), 2);
+      wait_vm(std::integral_constant<int, 4 * DQ>{});
+      __syncthreads();
+      f32x16 sa[2], sb[2];
+      qk(0, sa);
+      auto step = [&](int t, int buf, f32x16 (&cur)[2], f32x16 (&next)[2]) {
+        wait_vm(std::integral_constant<int, 2 * DQ>{});
+        __syncthreads();
+        fetch_dma(min((t + 3) * kBKV, last_kv), (buf + 3) & 3);
+        if (t + 1 < t_end) qk((buf + 1) & 3, next);
+        softmax_pv(t, buf, cur);
+      };
+      int t = t_begin, buf = 0;
+      for (; t + 1 < t_end; t += 2, buf = (buf + 2) & 3) {
+        step(t, buf, sa, sb);
+        step(t + 1, (buf + 1) & 3, sb, sa);
+      }
+      if (t < t_end) step(t, buf, sa, sb);
+      // no DMA may still target this workgroup's LDS when it retires
+      wait_vm(std::integral_constant<int, 0>{});
     }
-    if (t < t_end) tile(t, 0);
+  } else {
+    // Fetches are unconditional (past the end they re-read the last tile), so
+    // the wait before staging tile t+1 does not cover the loads of tile t+2.
+    auto tile = [&](int t, int r) {      // r = (t - t_begin) & 1 (a constant at each call site)
+      fetch(min(t * kBKV + 2 * kBKV, last_kv), r);
+      compute(t, r);
+      stage(r ^ 1, r ^ 1);
+      __syncthreads();
+    };
+    if (t_begin < t_end) {               // uniform over the workgroup
+      fetch(t_begin * kBKV, 0);
+      fetch(min((t_begin + 1) * kBKV, last_kv), 1);
+      stage(0, 0);
+      __syncthreads();
+      int t = t_begin;
+      for (; t + 1 < t_end; t += 2) {
+        tile(t, 0);
+        tile(t + 1, 1);
+      }
+      if (t < t_end) tile(t, 0);
+    }
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
