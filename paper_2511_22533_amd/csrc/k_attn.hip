@@ -58,6 +58,25 @@ __device__ __forceinline__ float max3(float a, float b, float c) {
   return r;
 }
 
+// Max of the 16 accumulators of one 32 x 32 score tile: eight dependent
+// v_max3_f32 in one block (one hazard boundary for the compiler instead of
+// one per instruction; dependent VALU instructions need no wait states).
+__device__ __forceinline__ float max16(const f32x16& v) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3\n\t"
+      "v_max3_f32 %0, %0, %4, %5\n\t"
+      "v_max3_f32 %0, %0, %6, %7\n\t"
+      "v_max3_f32 %0, %0, %8, %9\n\t"
+      "v_max3_f32 %0, %0, %10, %11\n\t"
+      "v_max3_f32 %0, %0, %12, %13\n\t"
+      "v_max3_f32 %0, %0, %14, %15\n\t"
+      "v_max_f32 %0, %0, %16"
+      : "=&v"(r)
+      : "v"(v[0]), "v"(v[1]), "v"(v[2]), "v"(v[3]), "v"(v[4]), "v"(v[5]), "v"(v[6]), "v"(v[7]), "v"(v[8]),
+        "v"(v[9]), "v"(v[10]), "v"(v[11]), "v"(v[12]), "v"(v[13]), "v"(v[14]), "v"(v[15]));
+  return r;
+}
+
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 constexpr float kRescaleLog2 = 8.0f;
@@ -272,17 +291,16 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
         for (int e = 0; e < 16; ++e)
           if (kv0 + kt * 32 + 8 * (e >> 2) + 4 * g + (e & 3) >= nk) sacc[kt][e] = -INFINITY;
     }
-    // Max over this lane's 32 scores: two independent chains of v_max3.
-    float ma = max3(sacc[0][0], sacc[0][1], sacc[0][2]), mb = max3(sacc[1][0], sacc[1][1], sacc[1][2]);
-#pragma unroll
-    for (int e = 3; e < 15; e += 2) {
-      ma = max3(ma, sacc[0][e], sacc[0][e + 1]);
-      mb = max3(mb, sacc[1][e], sacc[1][e + 1]);
-    }
-    float mx = max3(ma, mb, max3(sacc[0][15], sacc[1][15], -INFINITY));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    // Lazy rescale: move the reference max only when it grows by more than 2^8.
+    // Max over this lane's 32 scores (two independent v_max3 chains).
+    const float m0 = max16(sacc[0]), m1 = max16(sacc[1]);
+    float mx = max3(m0, m1, m1);
+    // Lazy rescale: move the reference max only when some score exceeds it by
+    // more than 2^8 (base 2). m_run is the same in lanes l and l ^ 32 (it only
+    // changes here, from the query's full max), so each lane tests its own
+    // 32 keys and the wave-wide vote covers the query's other 32; the
+    // exchange for the full max is needed only in the (rare) branch.
     if (__builtin_amdgcn_ballot_w64((mx - m_run) * c > kRescaleLog2) != 0) {
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
       const float m_new = fmaxf(m_run, mx);
       const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c);
       m_run = m_new;
