@@ -6,7 +6,14 @@ Readings where the paper is silent or loose:
   anchored at the step index ceil(T * rho_a));
 * Eq. (5) yields a real bound on the cached count; the integer quota is the
   largest integer not above it, clamped to [0, N];
-* Phase 3 with f_corr = 0 never forces a full step, f_corr = 1 always does.
+* Phase 3 with f_corr = 0 never forces a full step, f_corr = 1 always does;
+* Error Accumulation Elimination (tau): "consecutive caches" counts the
+  immediately preceding steps that ran with a non-empty cached set (a full
+  step resets it). Two readings of the threshold are kept: the cycle reading
+  of the prose (a full refresh every tau steps: tau - 1 cached steps, then a
+  forced full one, so tau = 1 never caches) and the literal reading of
+  Algorithm 1 (force a full step once tau cached steps have passed, so tau = 1
+  alternates). tau = 0 disables the constraint. It applies in every phase.
 """
 from __future__ import annotations
 
@@ -81,3 +88,38 @@ def phase_quota(k: int, steps: int, n_tokens: int, n_cache_phase2: int,
     if f_corr > 0 and (k_refine + 1) % f_corr == 0:
         return 0
     return int(math.floor(n_tokens * _exact(xi)))
+
+
+TAU_CYCLE = 0
+TAU_LITERAL = 1
+
+
+def tau_forces_full(consecutive: int, tau: int, reading: int = TAU_CYCLE) -> bool:
+    """Algorithm 1, SSC: whether the cached set is emptied after `consecutive`
+    cached steps in a row (see the module readings)."""
+    if tau <= 0:
+        return False
+    limit = tau - 1 if reading == TAU_CYCLE else tau
+    return consecutive >= limit
+
+
+def plan(steps: int, n_tokens: int, sigma: float, mu: float = -0.07, gamma_up: float = 1.0,
+         rho_a=0.2, rho_cfg_off=0.75, xi=0.7, f_corr: int = 3, tau: int = 0,
+         reading: int = TAU_CYCLE):
+    """Cached count c_k for k = 1..T, pre-calculated before the loop.
+
+    Step 1 of Algorithm 1 with the Phase 2 budget N_cache(t) from the predictive
+    curve (Eqs. 4-5, sigma measured at the anchor step ceil(T rho_a)), then the
+    Error Accumulation Elimination of the SSC function over the run of cached
+    steps.
+    """
+    k_anchor = anchor_step(steps, rho_a)
+    out, run = [], 0
+    for k in range(1, steps + 1):
+        c = phase_quota(k, steps, n_tokens, pcsc_quota(k, n_tokens, sigma, mu, k_anchor, gamma_up),
+                        rho_a, rho_cfg_off, xi, f_corr)
+        if c > 0 and tau_forces_full(run, tau, reading):
+            c = 0
+        run = run + 1 if c > 0 else 0
+        out.append(c)
+    return out

@@ -136,3 +136,67 @@ def test_flops_at_trellis_shape():
     # 24 blocks, width 1024, 16 heads, 1374 x 1024 condition tokens, 4096 tokens
     f = flops.forward_flops(synth.TRELLIS16, 4096)
     assert math.isclose(f / 1e12, 5.2744894464, rel_tol=1e-12)
+
+
+# ---------------------------------------------------------------- full plan
+
+def _cached(pattern_plan):
+    return [1 if c > 0 else 0 for c in pattern_plan]
+
+
+def test_plan_defaults_tau3_worked_by_hand():
+    # T = 25 with the default hyperparameters (rho_a 0.2, rho_CFG-OFF 0.75,
+    # xi 0.7, f_corr 3, tau 3, cycle reading): Phase 1 is k = 1..5, Phase 2
+    # k = 6..18, Phase 3 k = 19..25 with correction steps at k = 21 and 24.
+    # Worked by hand from Algorithm 1: two cached steps, then a refresh.
+    p = schedule.plan(25, 4096, sigma=100.0, tau=3)
+    want = [0] * 5 + [1, 1, 0, 1, 1, 0, 1, 1, 0, 1, 1, 0, 1] + [1, 0, 0, 1, 1, 0, 1]
+    assert _cached(p) == want
+    # Phase 3 cached steps use floor(4096 * 0.7) = 2867
+    assert p[18] == p[21] == p[22] == p[24] == 2867
+
+
+def test_plan_tau_extremes():
+    kw = dict(steps=25, n_tokens=4096, sigma=50.0)
+    assert schedule.plan(tau=1, **kw) == [0] * 25                      # cycle reading: never caches
+    lit = _cached(schedule.plan(tau=1, reading=schedule.TAU_LITERAL, **kw))
+    assert all(not (a and b) for a, b in zip(lit, lit[1:]))            # literal: never two cached in a row
+    assert sum(lit) > 0
+    base = schedule.plan(tau=0, **kw)
+    assert schedule.plan(tau=26, **kw) == base                         # a limit beyond T changes nothing
+    assert schedule.plan(tau=26, reading=schedule.TAU_LITERAL, **kw) == base
+
+
+def test_plan_literal_is_cycle_shifted_by_one():
+    # literal tau reads as the cycle reading with tau + 1 (both count the same run)
+    for tau in (1, 2, 3, 5, 8):
+        for f_corr in (0, 3):
+            kw = dict(steps=50, n_tokens=32768, sigma=900.0, mu=-0.05, gamma_up=4.0, f_corr=f_corr)
+            assert (schedule.plan(tau=tau, reading=schedule.TAU_LITERAL, **kw)
+                    == schedule.plan(tau=tau + 1, **kw))
+
+
+def test_plan_without_tau_is_phase_rule_with_pcsc():
+    T, N, sigma, mu, g = 25, 4096, 300.0, -0.07, 2.0
+    p = schedule.plan(T, N, sigma, mu=mu, gamma_up=g)
+    ka = schedule.anchor_step(T)
+    for k in range(1, T + 1):
+        if k <= ka or k == 21 or k == 24:
+            assert p[k - 1] == 0
+        elif k < 19:
+            # Eq. (5) closed form at the step index
+            assert p[k - 1] == math.floor(N - sigma * math.exp(mu * (k - ka)) / g)
+        else:
+            assert p[k - 1] == 2867
+
+
+def test_plan_runs_never_exceed_the_limit():
+    import itertools
+    for tau, reading in itertools.product((2, 3, 4, 7), (schedule.TAU_CYCLE, schedule.TAU_LITERAL)):
+        c = _cached(schedule.plan(40, 512, sigma=20.0, f_corr=0, tau=tau, reading=reading))
+        limit = tau - 1 if reading == schedule.TAU_CYCLE else tau
+        run = longest = 0
+        for v in c:
+            run = run + 1 if v else 0
+            longest = max(longest, run)
+        assert longest == limit          # Phase 2/3 are long enough to reach the limit
