@@ -276,6 +276,39 @@ int32_t f3c_pcsc_quota(int32_t k, int32_t n_tokens, double sigma, double mu, int
 int32_t f3c_phase_quota(int32_t k, int32_t steps, int32_t n_tokens, int32_t n_cache_phase2, double rho_a,
                         double rho_off, double xi, int32_t f_corr);
 
+/* Error Accumulation Elimination (Algorithm 1, SSC: the cached set is emptied
+ * once "consecutive caches >= tau"). consecutive counts the immediately
+ * preceding steps that ran with a non-empty cached set. Two readings:
+ * F3C_TAU_CYCLE, the prose's full refresh every tau steps (tau - 1 cached
+ * steps, then a full one; tau = 1 never caches), and F3C_TAU_LITERAL, the
+ * algorithm's threshold (tau cached steps, then a full one; tau = 1
+ * alternates). tau = 0 disables it. Returns 1 when the step must run full. */
+#define F3C_TAU_CYCLE 0
+#define F3C_TAU_LITERAL 1
+int32_t f3c_tau_forces_full(int32_t consecutive, int32_t tau, int32_t reading);
+
+/* Hyperparameters of the three-phase schedule (Sec. 4; defaults of the paper:
+ * rho_a 0.2, rho_off 0.75, xi 0.7, f_corr 3, mu -0.07, tau 3). */
+typedef struct {
+  int32_t steps;        /* T */
+  int32_t n_tokens;     /* N = D^3 */
+  double rho_a;         /* Phase 1 ends at step ceil(T rho_a) (the anchor) */
+  double rho_off;       /* Phase 3 starts at step ceil(T rho_CFG-OFF) */
+  double xi;            /* Phase 3 cached ratio */
+  int32_t f_corr;       /* Phase 3 correction period (0: none) */
+  double mu;            /* slope of the predictive curve (Eq. 4) */
+  double gamma_up;      /* latent-to-decoded volume factor of Eq. (5), > 0 */
+  int32_t tau;          /* Error Accumulation Elimination interval (0: off) */
+  int32_t tau_reading;  /* F3C_TAU_CYCLE or F3C_TAU_LITERAL */
+} f3c_schedule_cfg;
+
+/* The whole schedule, pre-calculated before the loop (Algorithm 1): for
+ * k = 1..T, n_cache_out[k-1] = the cached count of step k from the phase rule
+ * with the Phase 2 budget of Eqs. (4)-(5) (sigma: dynamic voxels measured at
+ * the anchor step), then the tau constraint over the run of cached steps.
+ * n_cache_out: host array of T ints. Returns F3C_EINVAL on bad parameters. */
+int f3c_schedule_plan(const f3c_schedule_cfg* cfg, double sigma, int32_t* n_cache_out);
+
 #ifdef __cplusplus
 }
 #endif

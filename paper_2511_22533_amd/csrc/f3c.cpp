@@ -849,4 +849,30 @@ int32_t f3c_phase_quota(int32_t k, int32_t steps, int32_t n_tokens, int32_t n_ca
   return (int32_t)std::floor(p + 1e-9 * (p > 1 ? p : 1));
 }
 
+int32_t f3c_tau_forces_full(int32_t consecutive, int32_t tau, int32_t reading) {
+  if (tau <= 0) return 0;
+  return consecutive >= (reading == F3C_TAU_LITERAL ? tau : tau - 1);
+}
+
+int f3c_schedule_plan(const f3c_schedule_cfg* c, double sigma, int32_t* n_cache_out) {
+  if (!c || !n_cache_out) return fail(F3C_EINVAL, "NULL argument");
+  if (c->steps < 1 || c->n_tokens < 1) return fail(F3C_EINVAL, "need steps >= 1 and n_tokens >= 1");
+  if (!std::isfinite(sigma) || !std::isfinite(c->mu) || !(c->gamma_up > 0) || !std::isfinite(c->gamma_up))
+    return fail(F3C_EINVAL, "sigma and mu must be finite and gamma_up positive");
+  if (!(c->rho_a >= 0 && c->rho_a <= 1) || !(c->rho_off >= 0 && c->rho_off <= 1) || !(c->xi >= 0 && c->xi <= 1))
+    return fail(F3C_EINVAL, "rho_a, rho_off and xi must lie in [0, 1]");
+  if (c->f_corr < 0 || c->tau < 0) return fail(F3C_EINVAL, "f_corr and tau must be >= 0");
+  if (c->tau_reading != F3C_TAU_CYCLE && c->tau_reading != F3C_TAU_LITERAL) return fail(F3C_EINVAL, "bad tau_reading");
+  const int32_t k_anchor = f3c_ceil_ratio(c->steps, c->rho_a);
+  int32_t run = 0;                    // cached steps in a row before step k
+  for (int32_t k = 1; k <= c->steps; ++k) {
+    const int32_t phase2 = f3c_pcsc_quota(k, c->n_tokens, sigma, c->mu, k_anchor, c->gamma_up);
+    int32_t n = f3c_phase_quota(k, c->steps, c->n_tokens, phase2, c->rho_a, c->rho_off, c->xi, c->f_corr);
+    if (n > 0 && f3c_tau_forces_full(run, c->tau, c->tau_reading)) n = 0;
+    run = n > 0 ? run + 1 : 0;
+    n_cache_out[k - 1] = n;
+  }
+  return F3C_OK;
+}
+
 }  // extern "C"

@@ -5,7 +5,7 @@
 //
 //   f3c_drive [--grid G] [--width D] [--depth L] [--heads H] [--cond NC]
 //             [--cond-width DC] [--f32] [--batch B] [--steps T] [--eta E]
-//             [--quotas c1,c2,...] [--repeat R] [--copy-mib M]
+//             [--quotas c1,c2,...] [--repeat R] [--copy-mib M] [--graph]
 //
 // Defaults: the 24-block, width-1024 bf16 model on a 16^3 grid with 1374 x
 // 1024 condition tokens, 25 steps with the eta = 3 time shift (Eq. S1), every
@@ -19,6 +19,10 @@
 //
 // --copy-mib M first runs one plain float4 copy of M MiB (k_copy_ref): a
 // known-size reference for hardware byte counters.
+//
+// --graph captures the T steps of a trajectory once into a HIP graph and
+// replays it; the per-trajectory cache reset (a memset), the copy of x_T and
+// the condition K/V stay eager launches before each replay.
 #include <hip/hip_runtime.h>
 
 #include <chrono>
@@ -103,6 +107,7 @@ int main(int argc, char** argv) {
   cfg.cond_width = 1024;
   cfg.dtype = F3C_BF16;
   int batch = 1, steps = 25, repeat = 1, copy_mib = 0;
+  bool use_graph = false;
   double eta = 3.0;
   std::vector<int> quotas;
   for (int i = 1; i < argc; ++i) {
@@ -124,6 +129,7 @@ int main(int argc, char** argv) {
     else if (a == "--quotas") quotas = parse_list(val());
     else if (a == "--repeat") repeat = std::atoi(val());
     else if (a == "--copy-mib") copy_mib = std::atoi(val());
+    else if (a == "--graph") use_graph = true;
     else die(("unknown argument " + a).c_str());
   }
   if (quotas.empty()) quotas.assign(steps, 0);
@@ -195,6 +201,28 @@ int main(int argc, char** argv) {
   check(f3c_time_grid(steps, eta, times.data()), "f3c_time_grid");
   std::vector<int32_t> qb(batch);
 
+  auto run_steps = [&]() {
+    for (int k = 0; k < steps; ++k) {
+      if (quotas[k] == 0) {
+        check(f3c_full_step(s, x, times[k], times[k + 1], st), "f3c_full_step");
+      } else {
+        for (int b = 0; b < batch; ++b) qb[b] = quotas[k];
+        check(f3c_cached_step(s, x, times[k], times[k + 1], qb.data(), st), "f3c_cached_step");
+      }
+    }
+  };
+  hipGraphExec_t gexec = nullptr;
+  if (use_graph) {
+    check(f3c_set_cond(s, cond, st), "f3c_set_cond");    // the steps check that a condition is set
+    hip_check(hipStreamSynchronize(st), "hipStreamSynchronize");
+    hipGraph_t graph;
+    hip_check(hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal), "hipStreamBeginCapture");
+    run_steps();
+    hip_check(hipStreamEndCapture(st, &graph), "hipStreamEndCapture");
+    hip_check(hipGraphInstantiate(&gexec, graph, nullptr, nullptr, 0), "hipGraphInstantiate");
+    hip_check(hipGraphDestroy(graph), "hipGraphDestroy");
+  }
+
   hipEvent_t e0, e1;
   hip_check(hipEventCreate(&e0), "hipEventCreate");
   hip_check(hipEventCreate(&e1), "hipEventCreate");
@@ -204,22 +232,18 @@ int main(int argc, char** argv) {
     check(f3c_state_reset(s, st), "f3c_state_reset");
     hip_check(hipMemcpyAsync(x, x0, nx * 4, hipMemcpyDeviceToDevice, st), "hipMemcpyAsync");
     check(f3c_set_cond(s, cond, st), "f3c_set_cond");
-    for (int k = 0; k < steps; ++k) {
-      if (quotas[k] == 0) {
-        check(f3c_full_step(s, x, times[k], times[k + 1], st), "f3c_full_step");
-      } else {
-        for (int b = 0; b < batch; ++b) qb[b] = quotas[k];
-        check(f3c_cached_step(s, x, times[k], times[k + 1], qb.data(), st), "f3c_cached_step");
-      }
-    }
+    if (use_graph) hip_check(hipGraphLaunch(gexec, st), "hipGraphLaunch");
+    else run_steps();
   }
   hip_check(hipEventRecord(e1, st), "hipEventRecord");
   hip_check(hipEventSynchronize(e1), "hipEventSynchronize");
   const double wall = std::chrono::duration<double>(std::chrono::steady_clock::now() - w0).count();
   float ms = 0.0f;
   hip_check(hipEventElapsedTime(&ms, e0, e1), "hipEventElapsedTime");
-  std::printf("f3c_drive: %d trajectories x %d steps, batch %d: %.3f ms per step (GPU), %.3f ms per step (wall)\n",
-              repeat, steps, batch, ms / (repeat * steps), wall * 1e3 / (repeat * steps));
+  std::printf("f3c_drive: %d trajectories x %d steps, batch %d%s: %.3f ms per step (GPU), %.3f ms per step (wall)\n",
+              repeat, steps, batch, use_graph ? ", graph replay" : "", ms / (repeat * steps),
+              wall * 1e3 / (repeat * steps));
+  if (gexec) hip_check(hipGraphExecDestroy(gexec), "hipGraphExecDestroy");
 
   f3c_state_destroy(s);
   f3c_model_destroy(m);

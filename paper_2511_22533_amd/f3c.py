@@ -82,6 +82,8 @@ _SIGS = {
     "f3c_ceil_ratio": (c_int, [c_int, c_d]),
     "f3c_pcsc_quota": (c_int, [c_int, c_int, c_d, c_d, c_int, c_d]),
     "f3c_phase_quota": (c_int, [c_int, c_int, c_int, c_int, c_d, c_d, c_d, c_int]),
+    "f3c_tau_forces_full": (c_int, [c_int, c_int, c_int]),
+    "f3c_schedule_plan": (c_int, [ctypes.c_void_p, c_d, P_i32]),
 }
 
 _lib: Optional[ctypes.CDLL] = None
@@ -158,6 +160,27 @@ def pcsc_quota(k, n_tokens, sigma, mu, k_anchor, gamma_up) -> int:
 
 def phase_quota(k, steps, n_tokens, n_cache_phase2, rho_a=0.2, rho_off=0.75, xi=0.7, f_corr=3) -> int:
     return int(lib().f3c_phase_quota(k, steps, n_tokens, n_cache_phase2, rho_a, rho_off, xi, f_corr))
+
+
+TAU_CYCLE, TAU_LITERAL = 0, 1
+
+
+class ScheduleCfg(ctypes.Structure):
+    _fields_ = [("steps", c_int), ("n_tokens", c_int), ("rho_a", c_d), ("rho_off", c_d), ("xi", c_d),
+                ("f_corr", c_int), ("mu", c_d), ("gamma_up", c_d), ("tau", c_int), ("tau_reading", c_int)]
+
+
+def tau_forces_full(consecutive: int, tau: int, reading: int = TAU_CYCLE) -> bool:
+    return bool(lib().f3c_tau_forces_full(consecutive, tau, reading))
+
+
+def schedule_plan(steps: int, n_tokens: int, sigma: float, mu: float = -0.07, gamma_up: float = 1.0,
+                  rho_a: float = 0.2, rho_off: float = 0.75, xi: float = 0.7, f_corr: int = 3, tau: int = 0,
+                  reading: int = TAU_CYCLE) -> np.ndarray:
+    c = ScheduleCfg(steps, n_tokens, rho_a, rho_off, xi, f_corr, mu, gamma_up, tau, reading)
+    out = (ctypes.c_int32 * steps)()
+    check(lib().f3c_schedule_plan(ctypes.byref(c), sigma, out))
+    return np.array(out[:], dtype=np.int32)
 
 
 def forward_flops(cfg, n_tok: int, batch: int = 1) -> float:

@@ -164,3 +164,27 @@ def test_bench_counter_traffic_lookup():
     v, why = bench.counter_traffic("attn_self", "trellis16_cached")
     # a figure while the kernel sources match the recorded hash, else a stated reason
     assert (isinstance(v, int) and v > 0) or (v is None and "changed" in why)
+
+
+@pytest.mark.parametrize("steps", [10, 25, 50])
+@pytest.mark.parametrize("tau,reading", [(0, 0), (1, 0), (1, 1), (2, 0), (3, 0), (3, 1), (5, 0), (8, 1)])
+@pytest.mark.parametrize("f_corr", [0, 1, 3])
+def test_schedule_plan_matches_oracle(steps, tau, reading, f_corr):
+    for n, sigma, mu, g, xi in [(512, 40.0, -0.07, 1.0, 0.7), (4096, 900.0, -0.05, 4.0, 0.55),
+                                (32768, 30000.0, -0.12, 64.0, 0.8), (4096, 1e7, -0.07, 1.0, 0.7)]:
+        got = f3c.schedule_plan(steps, n, sigma, mu=mu, gamma_up=g, xi=xi, f_corr=f_corr, tau=tau, reading=reading)
+        want = osched.plan(steps, n, sigma, mu=mu, gamma_up=g, xi=xi, f_corr=f_corr, tau=tau, reading=reading)
+        assert got.tolist() == want
+    for run in range(12):
+        assert f3c.tau_forces_full(run, tau, reading) == osched.tau_forces_full(run, tau, reading)
+
+
+def test_schedule_plan_validation(L):
+    with pytest.raises(f3c.F3CError):
+        f3c.schedule_plan(25, 4096, 10.0, gamma_up=0.0)
+    with pytest.raises(f3c.F3CError):
+        f3c.schedule_plan(25, 4096, 10.0, reading=7)
+    with pytest.raises(f3c.F3CError):
+        f3c.schedule_plan(0, 4096, 10.0)
+    with pytest.raises(f3c.F3CError):
+        f3c.schedule_plan(25, 4096, float("nan"))
