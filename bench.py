@@ -127,6 +127,8 @@ def hbm_sweep():
       merge+Euler   B*N*(32*4 + 4)            (x in/out, v in, v_new out, pos)
       LN+mod        rows*d*(4 + 2)            (f32 h in, bf16 out)
       modulation    the bf16 weights of the two timestep layers and all blocks' 6d outputs
+      pack_occ      B*V*(4 + 1/8)             (f32 logit per voxel in, one bit out)
+      dyn_voxels    B*V/4                     (two packed grids in, Eq. 1)
     Times are per launch with no host gaps (the launches of each size are
     captured in one graph). The select kernel runs one workgroup per sample
     (keys stay in LDS), so it cannot fill the chip below about 256 samples:
@@ -190,6 +192,16 @@ def hbm_sweep():
         ms = _graph_time_ms(torch, lambda: f3c.op_ln_mod(f3c.F3C_BF16, h, out, sh, sc), 20)
         add("ln_mod", f"rows={rows} d=1024", rows * 1024 * 6, ms)
         del h, out
+
+    for B, V in [(1, 64 ** 3), (16, 64 ** 3), (1, 256 ** 3), (8, 256 ** 3)]:
+        logits = torch.randn((B, V), device="cuda", generator=g)
+        bits = torch.empty((2, B, (V + 31) // 32), dtype=torch.int32, device="cuda")
+        ms = _graph_time_ms(torch, lambda: f3c.op_pack_occupancy(logits, bits[0]), 20)
+        add("pack_occ", f"B={B} V={V}", B * V * 4 + B * V // 8, ms)
+        counts = torch.empty((B,), dtype=torch.int64, device="cuda")
+        ms = _graph_time_ms(torch, lambda: f3c.op_dynamic_voxels(bits[0], bits[1], counts), 20)
+        add("dyn_voxels", f"B={B} V={V}", B * V // 4, ms)
+        del logits, bits
 
     mcfg = synth.TRELLIS16
     mm = f3c.Model(mcfg).load(synth.make_weights(mcfg, seed=0))

@@ -256,6 +256,23 @@ int f3c_op_euler(int32_t batch, int32_t n_tokens, float* x, const float* v_cache
                  const int32_t* pos, const int32_t* act_off_host, double t, double t_next, float* v_new,
                  f3c_stream stream);
 
+/* Occupancy of decoded grids (Sec. 3, voxels evolution): voxel n of grid b is
+ * occupied when logits[b][n] > 0 (NaN: unoccupied). bits receives the packed
+ * grid, 32 voxels per word: voxel n in bit n % 32 of word n / 32 (voxels in
+ * row-major order of the grid, tail bits zero). logits f32 [B][n_voxels],
+ * bits u32 [B][ceil(n_voxels / 32)], both device. batch 1..65535. */
+int f3c_op_pack_occupancy(int32_t batch, int64_t n_voxels, const float* logits, uint32_t* bits,
+                          f3c_stream stream);
+
+/* Dynamic voxels, Eq. (1): counts[b] = sum over voxels of O_next XOR O_prev,
+ * i.e. popcount of the XOR of the packed grids b of occ_next and occ_prev
+ * (u32 [B][n_words], device; tail bits must match, e.g. both zero as written
+ * by f3c_op_pack_occupancy). counts: int64 [B], device. The count of the
+ * grids decoded at the anchor step and the step before it is the sigma of
+ * the predictive schedule (f3c_schedule_plan). */
+int f3c_op_dynamic_voxels(int32_t batch, int64_t n_words, const uint32_t* occ_next, const uint32_t* occ_prev,
+                          int64_t* counts, f3c_stream stream);
+
 /* ----------------------------------------------------------- host schedules */
 
 /* Timestep grid t_k = shift(1 - (k-1)/T), k = 1..T+1 (Eq. S1 with factor eta;

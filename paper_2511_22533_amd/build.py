@@ -21,7 +21,7 @@ LIB = os.path.join(LIB_DIR, "libf3c.so")
 DRIVER = os.path.join(LIB_DIR, "f3c_drive")
 ROOT = os.path.dirname(HERE)
 
-SOURCES = ["k_select.hip", "k_rows.hip", "k_gemm.hip", "k_attn.hip", "f3c.cpp"]
+SOURCES = ["k_select.hip", "k_rows.hip", "k_gemm.hip", "k_attn.hip", "k_occupancy.hip", "f3c.cpp"]
 DRIVER_SOURCE = "f3c_drive.hip"
 
 FLAGS = [

@@ -2,10 +2,39 @@
 // fragment traits for the 32x32 matrix-core family, and small helpers.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace f3c {
+
+// Timing of one profiled library call. While it is set on this thread, every
+// kernel launch goes through AMD's extended launch, which stamps the events
+// with the kernels' own start and end: the first kernel of the call stamps
+// start, each kernel re-stamps stop. The pair then spans the call's kernels
+// without the host's dispatch gap in front of them.
+struct LaunchTimer {
+  hipEvent_t start = nullptr, stop = nullptr;
+  bool used = false;
+};
+
+inline LaunchTimer& launch_timer() {
+  static thread_local LaunchTimer t;
+  return t;
+}
+
+// Kernel launch used by every kernel of the library (same arguments as
+// hipLaunchKernelGGL).
+template <typename F, typename... Args>
+inline void launch(F kernel, dim3 grid, dim3 block, uint32_t shmem, hipStream_t s, Args... args) {
+  LaunchTimer& t = launch_timer();
+  if (!t.stop) {
+    hipLaunchKernelGGL(kernel, grid, block, shmem, s, args...);
+    return;
+  }
+  hipExtLaunchKernelGGL(kernel, grid, block, shmem, s, t.used ? nullptr : t.start, t.stop, 0u, args...);
+  t.used = true;
+}
 
 typedef __bf16 bf16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));

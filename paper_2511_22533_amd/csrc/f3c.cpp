@@ -12,6 +12,7 @@
 #include <vector>
 
 #include "../../include/f3c.h"
+#include "common.h"
 #include "kernels.h"
 
 using namespace f3c;
@@ -104,32 +105,45 @@ hipEvent_t take_event(f3c_state* s) {
     s->pool.pop_back();
     return e;
   }
+  // Timing only (no host data is published through these events): without
+  // the system-scope fence, recording one costs no cache writeback before the
+  // next kernel, which would otherwise be counted in the timed interval.
   hipEvent_t e = nullptr;
-  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
   return e;
 }
 
-// Records an event pair around one launch when profiling is on.
+// Times one call's kernels when profiling is on for its class: the launches
+// inside the scope stamp the event pair at their own start and end (see
+// LaunchTimer). A scope that launched nothing records both events in place.
 struct Scope {
   f3c_state* s;
   int cls;
   hipStream_t st;
-  hipEvent_t e1 = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  LaunchTimer saved;
   Scope(f3c_state* s_, int cls_, hipStream_t st_, double flops, double bytes) : s(s_), cls(cls_), st(st_) {
     if (!(s->prof_mask >> cls & 1u)) return;
-    hipEvent_t e0 = take_event(s);
+    e0 = take_event(s);
     e1 = take_event(s);
-    if (!e0 || !e1) { e1 = nullptr; return; }
-    (void)hipEventRecord(e0, st);
+    if (!e0 || !e1) { e0 = e1 = nullptr; return; }
     s->prof[cls].ev.push_back(e0);
+    s->prof[cls].ev.push_back(e1);
     s->prof[cls].launches += 1;
     s->prof[cls].flops += flops;
     s->prof[cls].bytes += bytes;
+    LaunchTimer& t = launch_timer();
+    saved = t;
+    t = LaunchTimer{e0, e1, false};
   }
   ~Scope() {
     if (!e1) return;
-    (void)hipEventRecord(e1, st);
-    s->prof[cls].ev.push_back(e1);
+    LaunchTimer& t = launch_timer();
+    if (!t.used) {
+      (void)hipEventRecord(e0, st);
+      (void)hipEventRecord(e1, st);
+    }
+    t = saved;
   }
 };
 
@@ -811,6 +825,23 @@ int f3c_op_euler(int32_t batch, int32_t n_tokens, float* x, const float* v_cache
       if (act.off[b + 1] - act.off[b] != n_tokens) return fail(F3C_EINVAL, "without pos every token is active");
   const float dtf = (float)(t - t_next);
   HIP_TRY(launch_euler(x, v_cache, v_act, pos, act, batch, n_tokens, dtf, v_new, (hipStream_t)stream));
+  return F3C_OK;
+}
+
+int f3c_op_pack_occupancy(int32_t batch, int64_t n_voxels, const float* logits, uint32_t* bits, f3c_stream stream) {
+  if (!logits || !bits) return fail(F3C_EINVAL, "NULL argument");
+  if (batch < 1 || batch > 65535) return fail(F3C_EINVAL, "batch must be in 1..65535");
+  if (n_voxels < 1 || n_voxels > (int64_t(1) << 36)) return fail(F3C_EINVAL, "n_voxels must be in 1..2^36");
+  HIP_TRY(launch_pack_occupancy(logits, batch, n_voxels, bits, (hipStream_t)stream));
+  return F3C_OK;
+}
+
+int f3c_op_dynamic_voxels(int32_t batch, int64_t n_words, const uint32_t* occ_next, const uint32_t* occ_prev,
+                          int64_t* counts, f3c_stream stream) {
+  if (!occ_next || !occ_prev || !counts) return fail(F3C_EINVAL, "NULL argument");
+  if (batch < 1 || batch > 65535) return fail(F3C_EINVAL, "batch must be in 1..65535");
+  if (n_words < 1) return fail(F3C_EINVAL, "n_words must be positive");
+  HIP_TRY(launch_dynamic_voxels(occ_next, occ_prev, batch, n_words, counts, (hipStream_t)stream));
   return F3C_OK;
 }
 

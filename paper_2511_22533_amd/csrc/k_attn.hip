@@ -11,12 +11,17 @@
 // B operand without any data movement; the K-slot order of P (keys
 // 8*(e/4) + 4*(l/32) + e%4) is matched when the V^T fragment is read.
 //
-// Pipelining: the next K/V tile is fetched into registers while the current
-// one is consumed, then written to the other LDS buffer (one barrier per
-// tile). Only the last, ragged tile is masked. The running max is updated
-// lazily: the accumulators are rescaled only when some query's max grows by
-// more than 2^8 (in base-2 units), which keeps every unnormalised probability
-// below 2^8 and the result unchanged up to rounding.
+// Pipelining. bf16 with 64-wide heads (the transformer's case): K and V tiles
+// go from global memory straight into four LDS buffers with 16-byte DMA loads
+// issued three tiles ahead, and the score product of tile t+1 is issued before
+// the softmax and PV product of tile t, so the matrix cores have independent
+// work while the vector unit runs the softmax. Other types and head sizes
+// fetch the next tile into registers while the current one is consumed and
+// write it to the other of two LDS buffers. One barrier per tile either way.
+// Only the last, ragged tile is masked. The running max is updated lazily:
+// the accumulators are rescaled only when some query's max grows by more than
+// 2^8 (in base-2 units), which keeps every unnormalised probability below 2^8
+// and the result unchanged up to rounding.
 //
 // Few query tiles (late cached steps: a few hundred active tokens) cannot fill
 // 256 CUs, so the key range may be split: each split writes its unnormalised
@@ -104,7 +109,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
   constexpr int ES = sizeof(T);
   constexpr int E = Mfma<T>::E;
   // bf16 with 64-wide heads: K and V tiles go global -> LDS directly (16-byte
-  // DMA loads, no registers) into three buffers, row-major with 128-byte rows
+  // DMA loads, no registers) into four buffers, row-major with 128-byte rows
   // whose 16-byte chunks are XOR-swizzled by row (conflict-free fragment
   // reads); V^T fragments come from the row-major V tile through the LDS
   // transpose read. Other types and head sizes stage through registers, with
@@ -507,14 +512,14 @@ template <typename T, int HD, int NW, int SITE>
 hipError_t launch_k(const AttnArgs& a, int tiles, hipStream_t s) {
   const dim3 block(64 * NW);
   if (a.splits == 1) {
-    hipLaunchKernelGGL((k_attn<T, HD, NW, SITE, false>), dim3(tiles * a.heads), block, 0, s, a);
+    launch((k_attn<T, HD, NW, SITE, false>), dim3(tiles * a.heads), block, 0, s, a);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL((k_attn<T, HD, NW, SITE, true>), dim3(tiles * a.heads * a.splits), block, 0, s, a);
+  launch((k_attn<T, HD, NW, SITE, true>), dim3(tiles * a.heads * a.splits), block, 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t n = (int64_t)a.rows * a.heads * (HD / 4);
-  hipLaunchKernelGGL((k_attn_combine<T, HD>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
+  launch((k_attn_combine<T, HD>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

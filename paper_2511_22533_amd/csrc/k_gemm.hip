@@ -310,7 +310,7 @@ template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, int EPI, int
 hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
   if (a.xq < 1 || (a.N / BN) % a.xq) return hipErrorInvalidValue;
   dim3 grid((a.N / BN) * ((a.M + BM - 1) / BM));
-  hipLaunchKernelGGL((k_gemm<T, BM, BN, WGM, WGN, STAGES, EPI, SITE, PF>), grid, dim3(64 * WGM * WGN), 0, s, a);
+  launch((k_gemm<T, BM, BN, WGM, WGN, STAGES, EPI, SITE, PF>), grid, dim3(64 * WGM * WGN), 0, s, a);
   return hipGetLastError();
 }
 
@@ -321,11 +321,11 @@ hipError_t launch_splitk(const GemmArgs& a, int splits, float* ws, hipStream_t s
   GemmArgs pa = a;
   pa.resid = ws;
   dim3 grid((a.N / 64) * ((a.M + 63) / 64), 1, splits);
-  hipLaunchKernelGGL((k_gemm<T, 64, 64, 2, 2, 2, EPI_PARTIAL, SITE, 2>), grid, dim3(256), 0, s, pa);
+  launch((k_gemm<T, 64, 64, 2, 2, 2, EPI_PARTIAL, SITE, 2>), grid, dim3(256), 0, s, pa);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t total4 = (int64_t)a.M * a.N / 4;
-  hipLaunchKernelGGL((k_splitk_reduce<T, EPI, SITE>), dim3((unsigned)((total4 + 255) / 256)), dim3(256), 0, s, a, ws,
+  launch((k_splitk_reduce<T, EPI, SITE>), dim3((unsigned)((total4 + 255) / 256)), dim3(256), 0, s, a, ws,
                      splits);
   return hipGetLastError();
 }

@@ -302,11 +302,11 @@ __global__ __launch_bounds__(256) void k_convert(const float* __restrict__ src, 
 #define F3C_NPL_LAUNCH(d, KERNEL, T, grid, s, ...)                                        \
   do {                                                                                     \
     switch ((d) / 64) {                                                                    \
-      case 2: hipLaunchKernelGGL((KERNEL<T, 2>), grid, dim3(256), 0, s, __VA_ARGS__); break;   \
-      case 4: hipLaunchKernelGGL((KERNEL<T, 4>), grid, dim3(256), 0, s, __VA_ARGS__); break;   \
-      case 8: hipLaunchKernelGGL((KERNEL<T, 8>), grid, dim3(256), 0, s, __VA_ARGS__); break;   \
-      case 16: hipLaunchKernelGGL((KERNEL<T, 16>), grid, dim3(256), 0, s, __VA_ARGS__); break; \
-      case 32: hipLaunchKernelGGL((KERNEL<T, 32>), grid, dim3(256), 0, s, __VA_ARGS__); break; \
+      case 2: launch((KERNEL<T, 2>), grid, dim3(256), 0, s, __VA_ARGS__); break;   \
+      case 4: launch((KERNEL<T, 4>), grid, dim3(256), 0, s, __VA_ARGS__); break;   \
+      case 8: launch((KERNEL<T, 8>), grid, dim3(256), 0, s, __VA_ARGS__); break;   \
+      case 16: launch((KERNEL<T, 16>), grid, dim3(256), 0, s, __VA_ARGS__); break; \
+      case 32: launch((KERNEL<T, 32>), grid, dim3(256), 0, s, __VA_ARGS__); break; \
       default: return hipErrorInvalidValue;                                                \
     }                                                                                      \
     return hipGetLastError();                                                              \
@@ -344,7 +344,7 @@ hipError_t launch_euler(float* x, const float* v_cache, const float* v_act, cons
                         int B, int N, float dt, float* v_new, hipStream_t s) {
   const int64_t n = (int64_t)B * N;
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_euler, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, x, v_cache, v_act, pos, act, B,
+  launch(k_euler, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, x, v_cache, v_act, pos, act, B,
                      N, dt, v_new);
   return hipGetLastError();
 }
@@ -355,10 +355,10 @@ hipError_t launch_gemv(int dt, const void* W, const float* bias, const float* x,
   dim3 grid((rows + per_block - 1) / per_block);
   const size_t lds = (size_t)K * sizeof(float);
   if (dt == DT_BF16)
-    hipLaunchKernelGGL(k_gemv<bf16>, grid, dim3(256), lds, s, (const bf16*)W, bias, x, t, in_mode, out_silu, rows,
+    launch(k_gemv<bf16>, grid, dim3(256), lds, s, (const bf16*)W, bias, x, t, in_mode, out_silu, rows,
                        K, y);
   else
-    hipLaunchKernelGGL(k_gemv<float>, grid, dim3(256), lds, s, (const float*)W, bias, x, t, in_mode, out_silu,
+    launch(k_gemv<float>, grid, dim3(256), lds, s, (const float*)W, bias, x, t, in_mode, out_silu,
                        rows, K, y);
   return hipGetLastError();
 }
@@ -368,9 +368,9 @@ hipError_t launch_gemv_t(int dt, const void* Wt, const float* bias, const float*
   const int per_block = 64 * (dt == DT_BF16 ? 8 : 4);
   dim3 grid((R + per_block - 1) / per_block);
   if (dt == DT_BF16)
-    hipLaunchKernelGGL(k_gemv_t<bf16>, grid, dim3(256), 0, s, (const bf16*)Wt, bias, x, R, K, y);
+    launch(k_gemv_t<bf16>, grid, dim3(256), 0, s, (const bf16*)Wt, bias, x, R, K, y);
   else
-    hipLaunchKernelGGL(k_gemv_t<float>, grid, dim3(256), 0, s, (const float*)Wt, bias, x, R, K, y);
+    launch(k_gemv_t<float>, grid, dim3(256), 0, s, (const float*)Wt, bias, x, R, K, y);
   return hipGetLastError();
 }
 
@@ -379,9 +379,9 @@ hipError_t launch_convert(int dt, const float* src, void* dst, int64_t n, hipStr
   const int64_t blocks = (n + 255) / 256;
   dim3 grid((unsigned)(blocks < 65536 ? blocks : 65536));
   if (dt == DT_BF16)
-    hipLaunchKernelGGL(k_convert<bf16>, grid, dim3(256), 0, s, src, (bf16*)dst, n);
+    launch(k_convert<bf16>, grid, dim3(256), 0, s, src, (bf16*)dst, n);
   else
-    hipLaunchKernelGGL(k_convert<float>, grid, dim3(256), 0, s, src, (float*)dst, n);
+    launch(k_convert<float>, grid, dim3(256), 0, s, src, (float*)dst, n);
   return hipGetLastError();
 }
 

@@ -248,7 +248,7 @@ __global__ __launch_bounds__(kThreads) void k_score_select(const float* __restri
 hipError_t launch_select(const float* v_cache, const float* v_prev, int B, int N, float w_a, float w_v,
                          const Segs& n_cache, const Segs& act, int32_t* idx_active, int32_t* pos,
                          float* score, hipStream_t s) {
-  hipLaunchKernelGGL(k_score_select, dim3(B), dim3(kThreads), 0, s, v_cache, v_prev, N, w_a, w_v, n_cache, act,
+  launch(k_score_select, dim3(B), dim3(kThreads), 0, s, v_cache, v_prev, N, w_a, w_v, n_cache, act,
                      idx_active, pos, score);
   return hipGetLastError();
 }

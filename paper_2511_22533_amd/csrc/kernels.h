@@ -82,4 +82,12 @@ hipError_t launch_attention(int site, int dt, int heads, int hd, const Segs& qs,
                             int ldq, const void* k, int ldk, const void* v, int ldv, void* o, int ldo, float* ws,
                             size_t ws_bytes, hipStream_t s);
 
+// Occupancy bits from decoder logits (occupied when > 0) for B grids of
+// n_voxels: bits [B][ceil(n_voxels / 32)] u32, voxel n in bit n % 32 of word n / 32.
+hipError_t launch_pack_occupancy(const float* logits, int B, int64_t n_voxels, uint32_t* bits, hipStream_t s);
+
+// counts[b] = popcount(a[b] ^ b[b]) over n_words words per grid (Eq. 1).
+hipError_t launch_dynamic_voxels(const uint32_t* a, const uint32_t* b, int B, int64_t n_words, int64_t* counts,
+                                 hipStream_t s);
+
 }  // namespace f3c

@@ -78,6 +78,8 @@ _SIGS = {
     "f3c_op_embed": (c_int, [c_p, c_int, c_p, c_p, P_i32, c_p, c_p]),
     "f3c_op_final": (c_int, [c_p, c_int, c_p, c_p, c_p]),
     "f3c_op_euler": (c_int, [c_int, c_int, c_p, c_p, c_p, c_p, P_i32, c_d, c_d, c_p, c_p]),
+    "f3c_op_pack_occupancy": (c_int, [c_int, c_i64, c_p, c_p, c_p]),
+    "f3c_op_dynamic_voxels": (c_int, [c_int, c_i64, c_p, c_p, c_p, c_p]),
     "f3c_time_grid": (c_int, [c_int, c_d, P_d]),
     "f3c_ceil_ratio": (c_int, [c_int, c_d]),
     "f3c_pcsc_quota": (c_int, [c_int, c_int, c_d, c_d, c_int, c_d]),
@@ -390,6 +392,24 @@ def op_euler(x, v_cache, v_act, pos, act_off, t: float, t_next: float, v_new, st
     B, N = x.shape[0], x.shape[1]
     check(lib().f3c_op_euler(B, N, x.data_ptr(), v_cache.data_ptr(), _ptr(v_act), _ptr(pos), _i32(act_off),
                              float(t), float(t_next), v_new.data_ptr(), _stream(stream)))
+
+
+def op_pack_occupancy(logits, bits, stream=None):
+    """logits f32 [B][n_voxels] -> bits int32/uint32 [B][ceil(n_voxels / 32)] (device tensors)."""
+    B, n = logits.shape[0], logits[0].numel()
+    if not (logits.is_contiguous() and bits.is_contiguous() and bits.numel() == B * ((n + 31) // 32)):
+        raise ValueError("logits [B][n] and bits [B][ceil(n/32)] must be contiguous")
+    check(lib().f3c_op_pack_occupancy(B, n, logits.data_ptr(), bits.data_ptr(), _stream(stream)))
+
+
+def op_dynamic_voxels(occ_next, occ_prev, counts, stream=None):
+    """Packed grids [B][n_words] (device) -> counts int64 [B] (device), Eq. (1)."""
+    B, n_words = occ_next.shape[0], occ_next[0].numel()
+    if not (occ_next.is_contiguous() and occ_prev.is_contiguous() and occ_prev.shape == occ_next.shape
+            and counts.numel() == B):
+        raise ValueError("occ_next, occ_prev [B][n_words] contiguous and counts [B] expected")
+    check(lib().f3c_op_dynamic_voxels(B, n_words, occ_next.data_ptr(), occ_prev.data_ptr(), counts.data_ptr(),
+                                      _stream(stream)))
 
 
 def op_ln_mod(dtype: int, h, out, shift=None, scale=None, stream=None):

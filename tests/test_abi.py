@@ -109,6 +109,13 @@ def test_op_entry_validation_is_host_side(L):
     assert L.f3c_op_euler(2, 16, 1, 2, 3, None, off, 1.0, 0.5, 5, None) == f3c.F3C_EINVAL  # pos NULL, partial
     assert L.f3c_op_euler(2, 16, 1, 2, None, 4, off, 1.0, 0.5, 5, None) == f3c.F3C_EINVAL  # rows but no v_act
     assert L.f3c_op_euler(2, 16, 1, 2, 3, 4, f3c._i32([0, 10, 5]), 1.0, 0.5, 5, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_pack_occupancy(1, 64, None, 1, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_pack_occupancy(0, 64, 1, 1, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_pack_occupancy(1, 0, 1, 1, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_pack_occupancy(65536, 64, 1, 1, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_dynamic_voxels(1, 2, 1, None, 1, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_dynamic_voxels(1, 0, 1, 1, 1, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_dynamic_voxels(0, 2, 1, 1, 1, None) == f3c.F3C_EINVAL
 
 
 @pytest.mark.parametrize("steps,eta", [(10, 1.0), (25, 3.0), (25, 2.0), (50, 1.5)])

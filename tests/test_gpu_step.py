@@ -214,3 +214,48 @@ def test_trellis16_trajectory_one_block(torch):
     err = rel_l2(x.cpu().numpy(), ref.x)
     say("trajectory rel L2", err)
     assert err < 3e-2
+
+
+def test_profiler_times_kernels_and_leaves_results_unchanged(torch):
+    """With every class profiled, launches go through the event-stamping
+    extended launch: the step's results stay bit-identical, every class that
+    launched has a positive time, and the class times fit inside the step's
+    wall time. The condition is long enough (1100 tokens) and the active set
+    small enough (112 tokens) that cross-attention splits its key range, so a
+    class of two kernels is timed too."""
+    from paper_2511_22533_amd import f3c
+    from paper_2511_22533_amd.f3c import PROF_CLASSES
+    cfg = synth.ModelConfig(grid=8, width=256, depth=2, heads=4, cond_tokens=1100, cond_width=64, dtype="bf16")
+    model = f3c.Model(cfg).load(synth.make_weights(cfg, seed=0))
+    state = f3c.State(model, 1)
+    cond = to_dev(synth.make_cond(cfg, 1))
+    x_T = synth.make_noise(cfg, 1)
+    outs = []
+    for profiled in (False, True):
+        say(f"profiled={profiled}")
+        state.reset()
+        state.set_cond(cond)
+        x = to_dev(x_T)
+        state.full_step(x, 1.0, 0.9)
+        state.full_step(x, 0.9, 0.8)
+        state.profile(True if profiled else None)
+        state.profile_reset()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        state.cached_step(x, 0.8, 0.7, [400])
+        e1.record()
+        torch.cuda.synchronize()
+        prof = state.profile_read()
+        state.profile(None)
+        outs.append(x.cpu().numpy())
+        if profiled:
+            want = {"select": 1, "embed": 1, "mod": 1, "ln": 3 * cfg.depth, "gemm_qkv": cfg.depth,
+                    "attn_self": cfg.depth, "gemm_o": cfg.depth, "gemm_q": cfg.depth, "attn_cross": cfg.depth,
+                    "gemm_co": cfg.depth, "gemm_fc1": cfg.depth, "gemm_fc2": cfg.depth, "final": 1, "euler": 1}
+            for c in PROF_CLASSES:
+                assert prof[c]["launches"] == want.get(c, 0), c
+                if want.get(c):
+                    assert prof[c]["ms"] > 0, c
+            total = sum(prof[c]["ms"] for c in PROF_CLASSES)
+            assert total <= e0.elapsed_time(e1) * 1.02 + 0.01
+    assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
