@@ -123,3 +123,16 @@ def plan(steps: int, n_tokens: int, sigma: float, mu: float = -0.07, gamma_up: f
         run = run + 1 if c > 0 else 0
         out.append(c)
     return out
+
+
+def cfg_active(t: float, lo: float = 0.5, hi: float = 1.0) -> bool:
+    """Classifier-free guidance applies at a step whose start time t lies in
+    the guidance interval [lo, hi] (the supplement's sampling configuration:
+    [0.5, 1] by default; [0, 1] is continuous guidance)."""
+    return lo <= float(t) <= hi
+
+
+def guided_steps(times, lo: float = 0.5, hi: float = 1.0) -> list:
+    """Per step k = 1..T (times t_1..t_{T+1}): whether step k is guided."""
+    return [cfg_active(t, lo, hi) for t in list(times)[:-1]]
+
