@@ -215,10 +215,11 @@ def hbm_sweep():
     print(json.dumps({"mode": "hbm_sweep", "peak_GB/s": PEAK_HBM_GBS, "rows": rows_out}), flush=True)
 
 
-def cpu_baseline(w, W, cond, x_T, quotas, times, depth):
+def cpu_baseline(w, W, cond, x_T, quotas, times, depth, guided=None):
     """Time the CPU oracle on a bounded sample: one full step and one cached step
     (the schedule's last quota), at `depth` blocks, scaled to the whole model and
-    interpolated over the schedule by the FLOPs model."""
+    interpolated over the schedule by the FLOPs model. A guided step counts as
+    two transformer passes (the oracle runs them one after the other)."""
     from oracle import dit, flops, sampler, ssc
     from paper_2511_22533_amd import synth
     cfg = w.model
@@ -245,11 +246,12 @@ def cpu_baseline(w, W, cond, x_T, quotas, times, depth):
     f_last = flops.forward_flops(cfg, N - n_last, 1)
     total = 0.0
     tokens = 0
-    for q in quotas:
+    for k, q in enumerate(quotas):
         n = N - int(q[0])
         f = flops.forward_flops(cfg, n, 1)
         frac = (f - f_last) / (f_full - f_last) if f_full > f_last else 1.0
-        total += scale * (t_cached + (t_full - t_cached) * frac)
+        passes = 2 if guided is not None and guided[k] else 1
+        total += passes * scale * (t_cached + (t_full - t_cached) * frac)
         tokens += n * w.batch
     steps = len(quotas)
     threads = len(os.sched_getaffinity(0))
@@ -260,7 +262,8 @@ def cpu_baseline(w, W, cond, x_T, quotas, times, depth):
         "kind": "oracle",
         "sample": (f"float64 NumPy oracle, {depth} of {cfg.depth} blocks: one full step ({N} tokens, "
                    f"{t_full:.2f} s) and one cached step ({N - n_last} active, {t_cached:.2f} s), scaled by "
-                   f"{scale:g} to all blocks and interpolated over the {steps}-step schedule with the FLOPs model"),
+                   f"{scale:g} to all blocks and interpolated over the {steps}-step schedule with the FLOPs model"
+                   + (f", guided steps counted as two passes ({sum(guided)} of {steps})" if guided is not None else "")),
         "active_tokens_per_s": tokens / total,
         "seconds_measured": t_full + t_cached,
     }
@@ -299,10 +302,12 @@ def main():
     quotas = synth.quota_schedule(w)
     times = f3c.time_grid(w.steps, w.shift)
     model = f3c.Model(cfg).load(W)
-    state = f3c.State(model, w.batch)
+    guided = [w.guidance > 0 and f3c.guidance_active(float(t), *w.guidance_interval) for t in times[:-1]]
+    state = f3c.State(model, w.batch, guided=any(guided))
     x = torch.empty((w.batch, cfg.tokens, cfg.in_ch), dtype=torch.float32, device="cuda")
     x_T_dev = torch.from_numpy(x_T).cuda()
     cond_dev = torch.from_numpy(cond).cuda()
+    uncond_dev = torch.from_numpy(synth.make_uncond(cfg, w.batch)).cuda() if any(guided) else None
     T = w.steps
 
     def run_step(i):
@@ -311,8 +316,12 @@ def main():
             state.reset()
             x.copy_(x_T_dev)
             state.set_cond(cond_dev)
+            if uncond_dev is not None:
+                state.set_uncond(uncond_dev)
         q = quotas[k].tolist()
-        if any(q):
+        if guided[k]:
+            state.guided_step(x, float(times[k]), float(times[k + 1]), q if any(q) else None, w.guidance)
+        elif any(q):
             state.cached_step(x, float(times[k]), float(times[k + 1]), q)
         else:
             state.full_step(x, float(times[k]), float(times[k + 1]))
@@ -347,7 +356,8 @@ def main():
     for i in range(args.steps):
         n_act = run_step(i)
         active += n_act
-        flop_total += sum(f3c.forward_flops(cfg, cfg.tokens - int(c), 1) for c in quotas[i % T])
+        flop_total += (2 if guided[i % T] else 1) * sum(f3c.forward_flops(cfg, cfg.tokens - int(c), 1)
+                                                         for c in quotas[i % T])
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     prof = state.profile_read()[dominant]
@@ -361,6 +371,8 @@ def main():
     x.copy_(x_T_dev)
     state.set_cond(cond_dev)
     full_ms = _event_time_ms(torch, lambda: state.full_step(x, float(times[0]), float(times[1])), 10)
+    guided_full_ms = _event_time_ms(torch, lambda: state.guided_step(x, float(times[0]), float(times[1]), None,
+                                                                     w.guidance), 10) if any(guided) else None
     k_min = int(np.argmax(quotas.sum(axis=1)))
     q_min = quotas[k_min].tolist()
     cached_ms = _event_time_ms(torch, lambda: state.cached_step(x, float(times[k_min]), float(times[k_min + 1]),
@@ -399,10 +411,12 @@ def main():
         "data": "synthetic (seeded weights, noise and condition tokens)",
         "config": {"workload": w.name, "grid": cfg.grid, "tokens": cfg.tokens, "width": cfg.width,
                    "depth": cfg.depth, "heads": cfg.heads, "cond_tokens": cfg.cond_tokens, "batch": w.batch,
-                   "steps_per_trajectory": T, "quota": w.schedule, "parallelism": "single GPU"},
+                   "steps_per_trajectory": T, "quota": w.schedule, "parallelism": "single GPU",
+                   **({"guidance": w.guidance, "guided_steps": int(sum(guided))} if any(guided) else {})},
         "active_tokens_per_s": round(active / elapsed, 1),
         "samples_per_s": round(w.batch * args.steps / elapsed / T, 3),
         "full_step_ms": round(full_ms, 4),
+        **({"guided_full_step_ms": round(guided_full_ms, 4)} if guided_full_ms is not None else {}),
         "cached_step_ms": round(cached_ms, 4) if cached_ms is not None else None,
         "cached_step_active_tokens": int(sum(cfg.tokens - c for c in q_min)),
         "step_model_tflops": round(step_tflops, 2),
@@ -411,7 +425,8 @@ def main():
     }
     if not args.no_cpu:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(w, W, cond, x_T, quotas, times, args.cpu_depth)
+        out["cpu_baseline"] = cpu_baseline(w, W, cond, x_T, quotas, times, args.cpu_depth,
+                                           guided if any(guided) else None)
     print(json.dumps(out), flush=True)
 
 

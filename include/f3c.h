@@ -44,6 +44,7 @@ extern "C" {
 #define F3C_BF16 1        /* bfloat16 operands, float32 accumulation and residual */
 
 #define F3C_MAX_BATCH 64
+#define F3C_STATE_GUIDED 1u   /* state flag: room for guided steps (two passes per sample) */
 #define F3C_MAX_TOKENS 32768
 
 typedef void* f3c_stream; /* hipStream_t */
@@ -112,6 +113,14 @@ int f3c_state_create(f3c_model* m, int32_t batch, void* state_dev, size_t bytes,
                      f3c_state** out);
 void f3c_state_destroy(f3c_state* s);
 
+/* As f3c_state_bytes / f3c_state_create with flags. F3C_STATE_GUIDED sizes the
+ * activations and the cross-attention keys/values for two transformer passes
+ * per sample (f3c_guided_step); batch is then at most F3C_MAX_BATCH / 2.
+ * Unknown flags: F3C_EINVAL. */
+int f3c_state_bytes_ex(const f3c_model* m, int32_t batch, uint32_t flags, size_t* bytes);
+int f3c_state_create_ex(f3c_model* m, int32_t batch, uint32_t flags, void* state_dev, size_t bytes,
+                        f3c_stream stream, f3c_state** out);
+
 /* Zero both velocity caches (start of a new trajectory). */
 int f3c_state_reset(f3c_state* s, f3c_stream stream);
 
@@ -122,6 +131,12 @@ int f3c_state_set_omega(f3c_state* s, float omega);
  * tokens cond_dev (float32 [B][Nc][dc], device). They depend only on the
  * condition and the weights, so one call serves the whole trajectory. */
 int f3c_set_cond(f3c_state* s, const float* cond_dev, f3c_stream stream);
+
+/* The unconditional input of classifier-free guidance (float32 [B][Nc][dc],
+ * device; an all-zero condition is the usual choice), precomputed like
+ * f3c_set_cond into the second half of the keys/values. Needs a state created
+ * with F3C_STATE_GUIDED (else F3C_ESTATE). */
+int f3c_set_uncond(f3c_state* s, const float* uncond_dev, f3c_stream stream);
 
 /* One denoising step of Algorithm 1 with every token active (Phase 1, Phase 3
  * correction steps): v = G(x_t, t, c); x <- x - (t - t_next) v; caches rotate.
@@ -136,6 +151,20 @@ int f3c_full_step(f3c_state* s, float* x_dev, double t, double t_next, f3c_strea
  * sample's active set; cached rows keep their stored velocity bit for bit.
  * With every n_cache_host[b] == 0 it computes exactly what f3c_full_step does. */
 int f3c_cached_step(f3c_state* s, float* x_dev, double t, double t_next, const int32_t* n_cache_host,
+                    f3c_stream stream);
+
+/* One guided step (classifier-free guidance inside the guidance interval; the
+ * supplement's sampling configuration uses t in [0.5, 1]). Selection as in
+ * f3c_cached_step (n_cache_host == NULL: every token active), scored from the
+ * stored guided velocities. The transformer runs twice on the same compacted
+ * active set (the single index set of Sec. 4.2), with the condition and with
+ * the unconditional input, as one batch of 2B sequences; the fresh velocity of
+ * an active token is fp32(1 + w) * v_cond - fp32(w) * v_uncond, each product
+ * and the difference rounded. Cached tokens keep their stored velocity. Needs a
+ * F3C_STATE_GUIDED state with f3c_set_cond and f3c_set_uncond done (else
+ * F3C_ESTATE); w finite. After the call, v_act (f3c_state_views) holds the
+ * conditional rows [sum n_b][8] followed by the unconditional ones. */
+int f3c_guided_step(f3c_state* s, float* x_dev, double t, double t_next, const int32_t* n_cache_host, double w,
                     f3c_stream stream);
 
 /* Device views of the state (valid until the next step call):
@@ -282,6 +311,11 @@ int f3c_time_grid(int32_t steps, double eta, double* out_host);
 /* ceil(steps * rho) for a decimal ratio rho (anchor step with rho_a, guidance-off
  * step with rho_CFG-OFF). */
 int32_t f3c_ceil_ratio(int32_t steps, double rho);
+
+/* Whether a step starting at time t is guided: 1 when lo <= t <= hi (the
+ * guidance interval of the supplement's sampling configuration, [0.5, 1] by
+ * default in TRELLIS; [0, 1] is continuous guidance), else 0. */
+int32_t f3c_guidance_active(double t, double lo, double hi);
 
 /* Eqs. (4)-(5): floor(N - sigma * exp(mu * (k - k_anchor)) / gamma_up) clamped to [0, N]. */
 int32_t f3c_pcsc_quota(int32_t k, int32_t n_tokens, double sigma, double mu, int32_t k_anchor, double gamma_up);

@@ -89,7 +89,8 @@ struct f3c_state {
   int32_t *idx, *pos;
   float* ws = nullptr;          // split-K partial sums
   size_t ws_bytes = 0;
-  bool cond_set = false, record_scores = false;
+  bool guided = false;          // activations and condition K/V sized for two passes per sample
+  bool cond_set = false, uncond_set = false, record_scores = false;
   uint32_t prof_mask = 0;
   float omega = 0.7f;
   Segs last_act{};
@@ -191,21 +192,35 @@ int check_state(f3c_state* s) {
   return F3C_OK;
 }
 
-int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_cache, hipStream_t st) {
+// One step of Algorithm 1. A guided step (guide) runs the transformer on two
+// copies of the compacted active set, the conditional pass in segments 0..B-1
+// and the unconditional one in segments B..2B-1 (same tokens, the second
+// condition's K/V), and merges (1 + w) v_cond - w v_uncond in the Euler kernel.
+int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_cache, bool guide, double w,
+             hipStream_t st) {
   f3c_model* m = s->m;
   const int B = s->B, N = m->N, d = m->d, L = m->L, dt = m->cfg.dtype;
   const size_t es = m->es;
-  Segs act{}, quota{}, cond_segs{};
-  act.B = quota.B = cond_segs.B = B;
+  Segs act{}, quota{};
+  act.B = quota.B = B;
   bool any_cached = false;
   for (int b = 0; b < B; ++b) {
     const int c = n_cache ? n_cache[b] : 0;
     quota.off[b] = c;
     act.off[b + 1] = act.off[b] + (N - c);
-    cond_segs.off[b + 1] = cond_segs.off[b] + m->Nc;
     any_cached |= c > 0;
   }
-  const int rows = act.off[B];
+  const int arows = act.off[B];              // active rows (one pass)
+  // Segments of the transformer: the active set once, or twice on a guided step.
+  const int P = guide ? 2 : 1;
+  Segs tact{}, cond_segs{};
+  tact.B = cond_segs.B = P * B;
+  for (int g = 0; g < P * B; ++g) {
+    const int b = g % B;
+    tact.off[g + 1] = tact.off[g] + (act.off[b + 1] - act.off[b]);
+    cond_segs.off[g + 1] = cond_segs.off[g] + m->Nc;
+  }
+  const int trows = tact.off[P * B];
   float* v_cache = s->v[s->cur];
   float* v_prev = s->v[1 - s->cur];
   const int32_t* idx = nullptr;
@@ -213,7 +228,7 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
 
   if (any_cached) {
     const float w_a = s->omega, w_v = 1.0f - w_a;
-    Scope sc(s, F3C_PROF_SELECT, st, 0, (double)B * N * (64 + 4) + rows * 4.0);
+    Scope sc(s, F3C_PROF_SELECT, st, 0, (double)B * N * (64 + 4) + arows * 4.0);
     HIP_TRY(launch_select(v_cache, v_prev, B, N, w_a, w_v, quota, act, s->idx, s->pos,
                           s->record_scores ? s->score : nullptr, st));
     idx = s->idx;
@@ -226,12 +241,14 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
     HIP_TRY(launch_gemv(dt, m->w("t2_w"), m->b("t2_b"), s->temb, 0.0, GEMV_IN_PLAIN, 0, d, d, s->temb + d, st));
     HIP_TRY(launch_gemv_t(dt, mw + m->mod_w, (const float*)(mw + m->mod_b), s->temb + d, 6 * L * d, d, s->mod, st));
   }
-  if (rows > 0) {
+  if (arows > 0) {
     {
-      Scope sc(s, F3C_PROF_EMBED, st, 0, rows * (32.0 + d * es + d * 4.0));
-      HIP_TRY(launch_embed(dt, x, N, idx, act, m->w("in_w"), m->b("in_b"), m->w("pos"), d, s->h, st));
+      Scope sc(s, F3C_PROF_EMBED, st, 0, arows * (32.0 + d * es + P * d * 4.0));
+      HIP_TRY(launch_embed(dt, x, N, idx, act, m->w("in_w"), m->b("in_b"), m->w("pos"), d, s->h, guide ? arows : 0,
+                           st));
     }
     const int dm = m->dm;
+    const int rows = trows;                    // the transformer's rows (both passes when guided)
     const double lnb = rows * (double)d * (4 + es);
     // Algorithmic bytes of the dense kernels (least data each must move):
     // projections read A and W and write the output (f32 residual read and
@@ -239,7 +256,7 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
     const double r = rows, dd = d, E = (double)es;
     auto proj_bytes = [&](double n, double k, bool resid) { return (r * k + n * k) * E + r * n * (resid ? 8.0 : E); };
     double cond_rows = 0;
-    for (int b = 0; b < B; ++b) cond_rows += (act.off[b + 1] > act.off[b]) ? m->Nc : 0;
+    for (int g = 0; g < P * B; ++g) cond_rows += (tact.off[g + 1] > tact.off[g]) ? m->Nc : 0;
     for (int l = 0; l < L; ++l) {
       const std::string p = "blk" + std::to_string(l) + ".";
       const float* md = s->mod + (size_t)l * 6 * d;
@@ -254,11 +271,12 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
       }
       {
         double fl = 0;
-        for (int b = 0; b < B; ++b) fl += 4.0 * (double)(act.off[b + 1] - act.off[b]) * (act.off[b + 1] - act.off[b]) * d;
+        for (int g = 0; g < P * B; ++g)
+          fl += 4.0 * (double)(tact.off[g + 1] - tact.off[g]) * (tact.off[g + 1] - tact.off[g]) * d;
         Scope sc(s, F3C_PROF_ATTN_SELF, st, fl, 4.0 * r * dd * E);
         const char* q = static_cast<const char*>(s->qkv);
-        HIP_TRY(launch_attention(SITE_SELF, dt, m->cfg.heads, m->hd, act, act, q, 3 * d, q + d * es, 3 * d, q + 2 * d * es,
-                                 3 * d, s->att, d, s->ws, s->ws_bytes, st));
+        HIP_TRY(launch_attention(SITE_SELF, dt, m->cfg.heads, m->hd, tact, tact, q, 3 * d, q + d * es, 3 * d,
+                                 q + 2 * d * es, 3 * d, s->att, d, s->ws, s->ws_bytes, st));
       }
       {
         Scope sc(s, F3C_PROF_GEMM_O, st, 2.0 * rows * d * d, proj_bytes(dd, dd, true));
@@ -277,8 +295,8 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
       {
         Scope sc(s, F3C_PROF_ATTN_CROSS, st, 4.0 * rows * m->Nc * d, (2.0 * r + 2.0 * cond_rows) * dd * E);
         const char* kv = static_cast<const char*>(s->kv) + (size_t)l * 2 * d * es;
-        HIP_TRY(launch_attention(SITE_CROSS, dt, m->cfg.heads, m->hd, act, cond_segs, s->qc, d, kv, 2 * L * d, kv + d * es,
-                                 2 * L * d, s->att, d, s->ws, s->ws_bytes, st));
+        HIP_TRY(launch_attention(SITE_CROSS, dt, m->cfg.heads, m->hd, tact, cond_segs, s->qc, d, kv, 2 * L * d,
+                                 kv + d * es, 2 * L * d, s->att, d, s->ws, s->ws_bytes, st));
       }
       {
         Scope sc(s, F3C_PROF_GEMM_CO, st, 2.0 * rows * d * d, proj_bytes(dd, dd, true));
@@ -306,9 +324,11 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
     }
   }
   {
-    Scope sc(s, F3C_PROF_EULER, st, 0, (double)B * N * 128 + rows * 32.0);
+    Scope sc(s, F3C_PROF_EULER, st, 0, (double)B * N * 128 + P * arows * 32.0);
     const float dtf = (float)(t - t_next);
-    HIP_TRY(launch_euler(x, v_cache, s->vact, pos, act, B, N, dtf, v_prev, st));
+    const float ga = (float)(1.0 + w), gw = (float)w;
+    HIP_TRY(launch_euler(x, v_cache, s->vact, guide ? s->vact + (size_t)arows * 8 : nullptr, ga, gw, pos, act, B, N,
+                         dtf, v_prev, st));
   }
   s->cur = 1 - s->cur;
   s->last_act = act;
@@ -470,60 +490,67 @@ double f3c_forward_flops(const f3c_model_cfg* c, int32_t n_tok, int32_t batch) {
                                 (double)c->width * c->mlp_ratio);
 }
 
-int f3c_state_bytes(const f3c_model* m, int32_t batch, size_t* bytes) {
+int f3c_state_bytes_ex(const f3c_model* m, int32_t batch, uint32_t flags, size_t* bytes) {
   if (!m || !bytes) return fail(F3C_EINVAL, "NULL argument");
-  if (batch < 1 || batch > F3C_MAX_BATCH) return fail(F3C_EINVAL, "batch must be in 1..%d", F3C_MAX_BATCH);
-  const size_t R = (size_t)batch * m->N, d = m->d, es = m->es;
+  if (flags & ~(uint32_t)F3C_STATE_GUIDED) return fail(F3C_EINVAL, "unknown state flags 0x%x", flags);
+  const int P = (flags & F3C_STATE_GUIDED) ? 2 : 1;
+  if (batch < 1 || batch * P > F3C_MAX_BATCH)
+    return fail(F3C_EINVAL, "batch must be in 1..%d%s", F3C_MAX_BATCH / P, P == 2 ? " for a guided state" : "");
+  const size_t R = (size_t)batch * m->N, A = P * R, d = m->d, es = m->es;
   size_t t = 0;
   t += 2 * align256(R * 32);                   // velocity cache pair
-  t += align256(R * d * 4);                    // h
-  t += 3 * align256(R * d * es);               // u, att, qc
-  t += align256(R * 3 * d * es);               // qkv
-  t += align256(R * m->dm * es);               // mlp hidden
-  t += align256(R * 32);                       // v_act
+  t += align256(A * d * 4);                    // h
+  t += 3 * align256(A * d * es);               // u, att, qc
+  t += align256(A * 3 * d * es);               // qkv
+  t += align256(A * m->dm * es);               // mlp hidden
+  t += align256(A * 32);                       // v_act
   t += 3 * align256(R * 4);                    // idx, pos, score
   t += align256((size_t)m->L * 6 * d * 4);     // mod
   t += align256(2 * d * 4);                    // temb scratch
-  t += align256((size_t)batch * m->Nc * m->dc * es);              // condition tokens
-  t += align256((size_t)batch * m->Nc * 2 * m->L * d * es);       // cross K/V, all blocks
-  t += kSplitWsBytes;                                               // split-K partials
+  t += align256((size_t)P * batch * m->Nc * m->dc * es);            // condition tokens
+  t += align256((size_t)P * batch * m->Nc * 2 * m->L * d * es);     // cross K/V, all blocks
+  t += kSplitWsBytes;                                                 // split-K partials
   *bytes = t;
   return F3C_OK;
 }
 
-int f3c_state_create(f3c_model* m, int32_t batch, void* state_dev, size_t bytes, f3c_stream stream,
-                     f3c_state** out) {
+int f3c_state_bytes(const f3c_model* m, int32_t batch, size_t* bytes) { return f3c_state_bytes_ex(m, batch, 0, bytes); }
+
+int f3c_state_create_ex(f3c_model* m, int32_t batch, uint32_t flags, void* state_dev, size_t bytes,
+                        f3c_stream stream, f3c_state** out) {
   if (!m || !state_dev || !out) return fail(F3C_EINVAL, "NULL argument");
   *out = nullptr;
   size_t need = 0;
-  int rc = f3c_state_bytes(m, batch, &need);
+  int rc = f3c_state_bytes_ex(m, batch, flags, &need);
   if (rc) return rc;
   if ((uintptr_t)state_dev & 255) return fail(F3C_EINVAL, "state buffer must be 256-byte aligned");
   if (bytes < need) return fail(F3C_ENOMEM, "state buffer %zu < %zu bytes", bytes, need);
   f3c_state* s = new f3c_state();
   s->m = m;
   s->B = batch;
+  s->guided = (flags & F3C_STATE_GUIDED) != 0;
   s->dev = static_cast<char*>(state_dev);
   s->bytes = bytes;
-  const size_t R = (size_t)batch * m->N, d = m->d, es = m->es;
+  const size_t P = s->guided ? 2 : 1;
+  const size_t R = (size_t)batch * m->N, A = P * R, d = m->d, es = m->es;
   char* p = s->dev;
   auto take = [&](size_t n) { char* r = p; p += align256(n); return r; };
   s->v[0] = (float*)take(R * 32);
   s->v[1] = (float*)take(R * 32);
-  s->h = (float*)take(R * d * 4);
-  s->u = take(R * d * es);
-  s->att = take(R * d * es);
-  s->qc = take(R * d * es);
-  s->qkv = take(R * 3 * d * es);
-  s->hid = take(R * m->dm * es);
-  s->vact = (float*)take(R * 32);
+  s->h = (float*)take(A * d * 4);
+  s->u = take(A * d * es);
+  s->att = take(A * d * es);
+  s->qc = take(A * d * es);
+  s->qkv = take(A * 3 * d * es);
+  s->hid = take(A * m->dm * es);
+  s->vact = (float*)take(A * 32);
   s->idx = (int32_t*)take(R * 4);
   s->pos = (int32_t*)take(R * 4);
   s->score = (float*)take(R * 4);
   s->mod = (float*)take((size_t)m->L * 6 * d * 4);
   s->temb = (float*)take(2 * d * 4);
-  s->cond_t = take((size_t)batch * m->Nc * m->dc * es);
-  s->kv = take((size_t)batch * m->Nc * 2 * m->L * d * es);
+  s->cond_t = take(P * batch * m->Nc * m->dc * es);
+  s->kv = take(P * batch * m->Nc * 2 * m->L * d * es);
   s->ws = (float*)take(kSplitWsBytes);
   s->ws_bytes = kSplitWsBytes;
   hipStream_t st = (hipStream_t)stream;
@@ -535,6 +562,11 @@ int f3c_state_create(f3c_model* m, int32_t batch, void* state_dev, size_t bytes,
   }
   *out = s;
   return F3C_OK;
+}
+
+int f3c_state_create(f3c_model* m, int32_t batch, void* state_dev, size_t bytes, f3c_stream stream,
+                     f3c_state** out) {
+  return f3c_state_create_ex(m, batch, 0, state_dev, bytes, stream, out);
 }
 
 void f3c_state_destroy(f3c_state* s) {
@@ -561,22 +593,45 @@ int f3c_state_set_omega(f3c_state* s, float omega) {
   return F3C_OK;
 }
 
+namespace {
+
+// Condition tokens of one pass ([B][Nc][dc] f32) -> the cross-attention K/V of
+// every block, stored at rows half * B * Nc of the state's K/V buffer.
+int cond_kv(f3c_state* s, const float* cond_dev, int half, hipStream_t st) {
+  f3c_model* m = s->m;
+  const int rows = s->B * m->Nc, n = 2 * m->L * m->d;
+  char* ct = static_cast<char*>(s->cond_t) + (size_t)half * rows * m->dc * m->es;
+  char* kv = static_cast<char*>(s->kv) + (size_t)half * rows * n * m->es;
+  Scope sc(s, F3C_PROF_COND, st, 2.0 * rows * n * m->dc, 0);
+  HIP_TRY(launch_convert(m->cfg.dtype, cond_dev, ct, (int64_t)rows * m->dc, st));
+  HIP_TRY(launch_gemm(SITE_COND, m->cfg.dtype, EPI_STORE, rows, n, m->dc, ct, m->dc, m->wdev + m->kv_w, m->dc,
+                      (const float*)(m->wdev + m->kv_b), nullptr, kv, n, nullptr, 0, s->ws, s->ws_bytes, st));
+  return F3C_OK;
+}
+
+}  // namespace
+
 int f3c_set_cond(f3c_state* s, const float* cond_dev, f3c_stream stream) {
   int rc = check_state(s);
   if (rc) return rc;
   if (!cond_dev) return fail(F3C_EINVAL, "cond is NULL");
-  f3c_model* m = s->m;
-  hipStream_t st = (hipStream_t)stream;
-  const int rows = s->B * m->Nc, n = 2 * m->L * m->d;
-  Scope sc(s, F3C_PROF_COND, st, 2.0 * rows * n * m->dc, 0);
-  HIP_TRY(launch_convert(m->cfg.dtype, cond_dev, s->cond_t, (int64_t)rows * m->dc, st));
-  HIP_TRY(launch_gemm(SITE_COND, m->cfg.dtype, EPI_STORE, rows, n, m->dc, s->cond_t, m->dc, m->wdev + m->kv_w, m->dc,
-                      (const float*)(m->wdev + m->kv_b), nullptr, s->kv, n, nullptr, 0, s->ws, s->ws_bytes, st));
+  if ((rc = cond_kv(s, cond_dev, 0, (hipStream_t)stream))) return rc;
   s->cond_set = true;
   return F3C_OK;
 }
 
-static int step_common(f3c_state* s, float* x, double t, double t_next, const int32_t* n_cache, f3c_stream stream) {
+int f3c_set_uncond(f3c_state* s, const float* uncond_dev, f3c_stream stream) {
+  int rc = check_state(s);
+  if (rc) return rc;
+  if (!s->guided) return fail(F3C_ESTATE, "state was not created with F3C_STATE_GUIDED");
+  if (!uncond_dev) return fail(F3C_EINVAL, "uncond is NULL");
+  if ((rc = cond_kv(s, uncond_dev, 1, (hipStream_t)stream))) return rc;
+  s->uncond_set = true;
+  return F3C_OK;
+}
+
+static int step_common(f3c_state* s, float* x, double t, double t_next, const int32_t* n_cache, bool guide, double w,
+                       f3c_stream stream) {
   int rc = check_state(s);
   if (rc) return rc;
   if (!s->cond_set) return fail(F3C_ESTATE, "condition not set (call f3c_set_cond first)");
@@ -587,17 +642,27 @@ static int step_common(f3c_state* s, float* x, double t, double t_next, const in
     for (int b = 0; b < s->B; ++b)
       if (n_cache[b] < 0 || n_cache[b] > s->m->N)
         return fail(F3C_EINVAL, "n_cache[%d] = %d outside [0, %d]", b, n_cache[b], s->m->N);
-  return run_step(s, x, t, t_next, n_cache, (hipStream_t)stream);
+  if (guide) {
+    if (!s->guided) return fail(F3C_ESTATE, "state was not created with F3C_STATE_GUIDED");
+    if (!s->uncond_set) return fail(F3C_ESTATE, "unconditional input not set (call f3c_set_uncond first)");
+    if (!std::isfinite(w)) return fail(F3C_EINVAL, "guidance weight must be finite");
+  }
+  return run_step(s, x, t, t_next, n_cache, guide, w, (hipStream_t)stream);
 }
 
 int f3c_full_step(f3c_state* s, float* x_dev, double t, double t_next, f3c_stream stream) {
-  return step_common(s, x_dev, t, t_next, nullptr, stream);
+  return step_common(s, x_dev, t, t_next, nullptr, false, 0.0, stream);
 }
 
 int f3c_cached_step(f3c_state* s, float* x_dev, double t, double t_next, const int32_t* n_cache_host,
                     f3c_stream stream) {
   if (!n_cache_host) return fail(F3C_EINVAL, "n_cache is NULL");
-  return step_common(s, x_dev, t, t_next, n_cache_host, stream);
+  return step_common(s, x_dev, t, t_next, n_cache_host, false, 0.0, stream);
+}
+
+int f3c_guided_step(f3c_state* s, float* x_dev, double t, double t_next, const int32_t* n_cache_host, double w,
+                    f3c_stream stream) {
+  return step_common(s, x_dev, t, t_next, n_cache_host, true, w, stream);
 }
 
 int f3c_state_views(const f3c_state* s, float** v_cache, float** v_prev, int32_t** idx_active, int32_t** pos,
@@ -799,7 +864,7 @@ int f3c_op_embed(const f3c_model* m, int32_t batch, const float* x, const int32_
     for (int b = 0; b < batch; ++b)
       if (act.off[b + 1] - act.off[b] != m->N) return fail(F3C_EINVAL, "without idx_active every token is active");
   HIP_TRY(launch_embed(m->cfg.dtype, x, m->N, idx_active, act, m->w("in_w"), m->b("in_b"), m->w("pos"), m->d, h,
-                       (hipStream_t)stream));
+                       0, (hipStream_t)stream));
   return F3C_OK;
 }
 
@@ -824,7 +889,8 @@ int f3c_op_euler(int32_t batch, int32_t n_tokens, float* x, const float* v_cache
     for (int b = 0; b < batch; ++b)
       if (act.off[b + 1] - act.off[b] != n_tokens) return fail(F3C_EINVAL, "without pos every token is active");
   const float dtf = (float)(t - t_next);
-  HIP_TRY(launch_euler(x, v_cache, v_act, pos, act, batch, n_tokens, dtf, v_new, (hipStream_t)stream));
+  HIP_TRY(launch_euler(x, v_cache, v_act, nullptr, 0.0f, 0.0f, pos, act, batch, n_tokens, dtf, v_new,
+                       (hipStream_t)stream));
   return F3C_OK;
 }
 
@@ -855,6 +921,8 @@ int f3c_time_grid(int32_t steps, double eta, double* out_host) {
   for (int k = 0; k <= steps; ++k) out_host[k] = shift_time(1.0 - (double)k / steps, eta);
   return F3C_OK;
 }
+
+int32_t f3c_guidance_active(double t, double lo, double hi) { return (lo <= t && t <= hi) ? 1 : 0; }
 
 int32_t f3c_ceil_ratio(int32_t steps, double rho) {
   const double p = steps * rho;

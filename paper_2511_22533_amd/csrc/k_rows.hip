@@ -19,7 +19,7 @@ template <typename T, int NPL>
 __global__ __launch_bounds__(256) void k_embed(const float* __restrict__ x, int N, const int32_t* __restrict__ idx,
                                                Segs act, const T* __restrict__ w_in,
                                                const float* __restrict__ b_in, const T* __restrict__ ptab,
-                                               float* __restrict__ h) {
+                                               float* __restrict__ h, int64_t dup) {
   constexpr int D = NPL * 64;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
@@ -40,7 +40,9 @@ __global__ __launch_bounds__(256) void k_embed(const float* __restrict__ x, int 
     float acc = 0.0f;
 #pragma unroll
     for (int c = 0; c < 8; ++c) acc += xv[c] * to_f32(w[c]);
-    hr[n] = acc + b_in[n] + to_f32(pr[n]);
+    const float e = acc + b_in[n] + to_f32(pr[n]);
+    hr[n] = e;
+    if (dup) hr[dup * D + n] = e;           // the unconditional pass's copy of the row
   }
 }
 
@@ -161,9 +163,18 @@ __global__ __launch_bounds__(256) void k_final(const float* __restrict__ h, int 
 
 // ------------------------------------------------------ merge + Euler + rotate
 // Algorithm 1 state update: v = v_cache; v[I_active] = v_active; S <- S - (t - t') v;
-// the new v is written to the other half of the cache ping-pong pair.
+// the new v is written to the other half of the cache ping-pong pair. On a
+// guided step (v_unc set) the fresh velocity of an active row is
+// ga * v_cond - gw * v_uncond, ga = fp32(1 + w), gw = fp32(w), each product
+// and the difference rounded (classifier-free guidance).
+__device__ __forceinline__ float4 guide4(float4 c, float4 u, float ga, float gw) {
+  return make_float4(__fsub_rn(__fmul_rn(ga, c.x), __fmul_rn(gw, u.x)), __fsub_rn(__fmul_rn(ga, c.y), __fmul_rn(gw, u.y)),
+                     __fsub_rn(__fmul_rn(ga, c.z), __fmul_rn(gw, u.z)), __fsub_rn(__fmul_rn(ga, c.w), __fmul_rn(gw, u.w)));
+}
+
 __global__ __launch_bounds__(256) void k_euler(float* __restrict__ x, const float* __restrict__ v_cache,
-                                               const float* __restrict__ v_act, const int32_t* __restrict__ pos,
+                                               const float* __restrict__ v_act, const float* __restrict__ v_unc,
+                                               float ga, float gw, const int32_t* __restrict__ pos,
                                                Segs act, int B, int N, float dt, float* __restrict__ v_new) {
 #pragma clang fp contract(off)
   const int64_t tok = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -172,7 +183,12 @@ __global__ __launch_bounds__(256) void k_euler(float* __restrict__ x, const floa
   const int i = (int)(tok - (int64_t)b * N);
   const int p = pos ? pos[tok] : act.off[b] + i;
   const float4* src = reinterpret_cast<const float4*>(p >= 0 ? v_act + (size_t)p * 8 : v_cache + tok * 8);
-  const float4 v0 = src[0], v1 = src[1];
+  float4 v0 = src[0], v1 = src[1];
+  if (v_unc && p >= 0) {
+    const float4* un = reinterpret_cast<const float4*>(v_unc + (size_t)p * 8);
+    v0 = guide4(v0, un[0], ga, gw);
+    v1 = guide4(v1, un[1], ga, gw);
+  }
   float4* xr = reinterpret_cast<float4*>(x + tok * 8);
   float4 x0 = xr[0], x1 = xr[1];
   x0.x = __fsub_rn(x0.x, __fmul_rn(dt, v0.x));
@@ -315,13 +331,15 @@ __global__ __launch_bounds__(256) void k_convert(const float* __restrict__ src, 
 }  // namespace
 
 hipError_t launch_embed(int dt, const float* x, int N, const int32_t* idx, const Segs& act, const void* w_in,
-                        const float* b_in, const void* pos_table, int d, float* h, hipStream_t s) {
+                        const float* b_in, const void* pos_table, int d, float* h, int64_t dup, hipStream_t s) {
   const int rows = act.off[act.B];
   if (rows == 0) return hipSuccess;
   dim3 grid((rows + 3) / 4);
   if (dt == DT_BF16)
-    F3C_NPL_LAUNCH(d, k_embed, bf16, grid, s, x, N, idx, act, (const bf16*)w_in, b_in, (const bf16*)pos_table, h);
-  F3C_NPL_LAUNCH(d, k_embed, float, grid, s, x, N, idx, act, (const float*)w_in, b_in, (const float*)pos_table, h);
+    F3C_NPL_LAUNCH(d, k_embed, bf16, grid, s, x, N, idx, act, (const bf16*)w_in, b_in, (const bf16*)pos_table, h,
+                   dup);
+  F3C_NPL_LAUNCH(d, k_embed, float, grid, s, x, N, idx, act, (const float*)w_in, b_in, (const float*)pos_table, h,
+                 dup);
 }
 
 hipError_t launch_ln_mod(int dt, const float* h, int rows, int d, const float* shift, const float* scale, void* out,
@@ -340,12 +358,12 @@ hipError_t launch_final(int dt, const float* h, int rows, int d, const void* w_o
   F3C_NPL_LAUNCH(d, k_final, float, grid, s, h, rows, (const float*)w_out, b_out, v_act);
 }
 
-hipError_t launch_euler(float* x, const float* v_cache, const float* v_act, const int32_t* pos, const Segs& act,
-                        int B, int N, float dt, float* v_new, hipStream_t s) {
+hipError_t launch_euler(float* x, const float* v_cache, const float* v_act, const float* v_unc, float ga, float gw,
+                        const int32_t* pos, const Segs& act, int B, int N, float dt, float* v_new, hipStream_t s) {
   const int64_t n = (int64_t)B * N;
   if (n == 0) return hipSuccess;
-  launch(k_euler, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, x, v_cache, v_act, pos, act, B,
-                     N, dt, v_new);
+  launch(k_euler, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, x, v_cache, v_act, v_unc, ga, gw, pos, act, B,
+         N, dt, v_new);
   return hipGetLastError();
 }
 

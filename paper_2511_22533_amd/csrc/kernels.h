@@ -32,10 +32,11 @@ hipError_t launch_select(const float* v_cache, const float* v_prev, int B, int N
                          const Segs& n_cache, const Segs& act, int32_t* idx_active, int32_t* pos,
                          float* score, hipStream_t s);
 
-// h[r][:] = x[b][i][:] W_in^T + b_in + P[i][:], i = idx_active[r] (identity when idx == nullptr).
+// h[r][:] = x[b][i][:] W_in^T + b_in + P[i][:], i = idx_active[r] (identity when idx == nullptr);
+// with dup > 0 the row is also written to h[r + dup] (the unconditional pass of a guided step).
 hipError_t launch_embed(int dt, const float* x, int N, const int32_t* idx, const Segs& act,
                         const void* w_in, const float* b_in, const void* pos_table, int d, float* h,
-                        hipStream_t s);
+                        int64_t dup, hipStream_t s);
 
 // out = LN(h) * (1 + scale) + shift, written as the model dtype; scale/shift may be null.
 hipError_t launch_ln_mod(int dt, const float* h, int rows, int d, const float* shift, const float* scale,
@@ -46,9 +47,11 @@ hipError_t launch_final(int dt, const float* h, int rows, int d, const void* w_o
                         float* v_act, hipStream_t s);
 
 // Merge + Euler + rotate: v = (pos >= 0 ? v_act[pos] : v_cache); x -= dt * v; v_new = v.
-// pos == nullptr means every token active at row act.off[b] + i.
-hipError_t launch_euler(float* x, const float* v_cache, const float* v_act, const int32_t* pos,
-                        const Segs& act, int B, int N, float dt, float* v_new, hipStream_t s);
+// pos == nullptr means every token active at row act.off[b] + i. With v_unc (guided step), an
+// active row's v is ga * v_act[p] - gw * v_unc[p], each operation rounded.
+hipError_t launch_euler(float* x, const float* v_cache, const float* v_act, const float* v_unc, float ga,
+                        float gw, const int32_t* pos, const Segs& act, int B, int N, float dt, float* v_new,
+                        hipStream_t s);
 
 // y[r] = W[r] . f(x) + b[r] (then SiLU when out_silu), f = identity / SiLU, or
 // x := the K sinusoidal features of t. K must be a multiple of 16 / sizeof(element).

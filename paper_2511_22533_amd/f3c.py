@@ -22,6 +22,7 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "f3c.h")
 
 F3C_OK, F3C_EINVAL, F3C_ENOMEM, F3C_EHIP, F3C_ESTATE = 0, -1, -2, -3, -4
 F3C_F32, F3C_BF16 = 0, 1
+F3C_STATE_GUIDED = 1
 PROF_CLASSES = ["select", "embed", "mod", "ln", "gemm_qkv", "attn_self", "gemm_o", "gemm_q", "attn_cross",
                 "gemm_co", "gemm_fc1", "gemm_fc2", "final", "euler", "cond"]
 
@@ -55,6 +56,11 @@ _SIGS = {
     "f3c_forward_flops": (c_d, [ctypes.POINTER(ModelCfg), c_int, c_int]),
     "f3c_state_bytes": (c_int, [c_p, c_int, ctypes.POINTER(c_sz)]),
     "f3c_state_create": (c_int, [c_p, c_int, c_p, c_sz, c_p, ctypes.POINTER(c_p)]),
+    "f3c_state_bytes_ex": (c_int, [c_p, c_int, ctypes.c_uint32, ctypes.POINTER(c_sz)]),
+    "f3c_state_create_ex": (c_int, [c_p, c_int, ctypes.c_uint32, c_p, c_sz, c_p, ctypes.POINTER(c_p)]),
+    "f3c_set_uncond": (c_int, [c_p, c_p, c_p]),
+    "f3c_guided_step": (c_int, [c_p, c_p, c_d, c_d, P_i32, c_d, c_p]),
+    "f3c_guidance_active": (c_int, [c_d, c_d, c_d]),
     "f3c_state_destroy": (None, [c_p]),
     "f3c_state_reset": (c_int, [c_p, c_p]),
     "f3c_state_set_omega": (c_int, [c_p, c_f]),
@@ -172,6 +178,10 @@ class ScheduleCfg(ctypes.Structure):
                 ("f_corr", c_int), ("mu", c_d), ("gamma_up", c_d), ("tau", c_int), ("tau_reading", c_int)]
 
 
+def guidance_active(t: float, lo: float = 0.5, hi: float = 1.0) -> bool:
+    return bool(lib().f3c_guidance_active(t, lo, hi))
+
+
 def tau_forces_full(consecutive: int, tau: int, reading: int = TAU_CYCLE) -> bool:
     return bool(lib().f3c_tau_forces_full(consecutive, tau, reading))
 
@@ -246,18 +256,22 @@ class Model:
 
 
 class State:
-    """A sampler state (velocity caches, activations, condition K/V) of one model."""
+    """A sampler state (velocity caches, activations, condition K/V) of one model.
 
-    def __init__(self, model: Model, batch: int, stream=None):
+    guided=True sizes it for guided steps (two transformer passes per sample)."""
+
+    def __init__(self, model: Model, batch: int, stream=None, guided: bool = False):
         import torch
-        self.model, self.batch = model, batch
+        self.model, self.batch, self.guided = model, batch, guided
+        flags = F3C_STATE_GUIDED if guided else 0
         b = c_sz()
-        check(lib().f3c_state_bytes(model.h, batch, ctypes.byref(b)))
+        check(lib().f3c_state_bytes_ex(model.h, batch, flags, ctypes.byref(b)))
         self.buf = torch.empty(b.value, dtype=torch.uint8, device="cuda")
         h = c_p()
-        check(lib().f3c_state_create(model.h, batch, self.buf.data_ptr(), self.buf.numel(), _stream(stream),
-                                     ctypes.byref(h)))
+        check(lib().f3c_state_create_ex(model.h, batch, flags, self.buf.data_ptr(), self.buf.numel(),
+                                        _stream(stream), ctypes.byref(h)))
         self.h = h
+        self.last_guided = False
 
     def reset(self, stream=None):
         check(lib().f3c_state_reset(self.h, _stream(stream)))
@@ -268,11 +282,22 @@ class State:
     def set_cond(self, cond, stream=None):
         check(lib().f3c_set_cond(self.h, cond.data_ptr(), _stream(stream)))
 
+    def set_uncond(self, uncond, stream=None):
+        check(lib().f3c_set_uncond(self.h, uncond.data_ptr(), _stream(stream)))
+
     def full_step(self, x, t: float, t_next: float, stream=None):
         check(lib().f3c_full_step(self.h, x.data_ptr(), t, t_next, _stream(stream)))
+        self.last_guided = False
 
     def cached_step(self, x, t: float, t_next: float, n_cache: Sequence[int], stream=None):
         check(lib().f3c_cached_step(self.h, x.data_ptr(), t, t_next, _i32(n_cache), _stream(stream)))
+        self.last_guided = False
+
+    def guided_step(self, x, t: float, t_next: float, n_cache: Optional[Sequence[int]], w: float, stream=None):
+        """Guided step; n_cache None runs every token."""
+        check(lib().f3c_guided_step(self.h, x.data_ptr(), t, t_next, None if n_cache is None else _i32(n_cache), w,
+                                    _stream(stream)))
+        self.last_guided = True
 
     def record_scores(self, on: bool):
         check(lib().f3c_state_record_scores(self.h, int(on)))
@@ -306,7 +331,9 @@ class State:
             "v_prev": view(v["v_prev"], B * N * 8, torch.float32, (B, N, 8)),
             "idx_active": view(v["idx_active"], rows, torch.int32, (rows,)),
             "pos": view(v["pos"], B * N, torch.int32, (B, N)),
-            "v_act": view(v["v_act"], rows * 8, torch.float32, (rows, 8)),
+            # a guided step leaves the conditional rows followed by the unconditional ones
+            "v_act": view(v["v_act"], (2 if self.last_guided else 1) * rows * 8, torch.float32,
+                          ((2 if self.last_guided else 1) * rows, 8)),
             "mod": view(v["mod"], cfg.depth * 6 * cfg.width, torch.float32, (cfg.depth, 6, cfg.width)),
             "score": view(v["score"], B * N, torch.float32, (B, N)),
             "act_off": v["act_off"],

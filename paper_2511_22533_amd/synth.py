@@ -67,6 +67,8 @@ class Workload:
     shift: float                # timestep shift factor eta (1.0 = uniform)
     schedule: str               # quota recipe name, see ``quota_schedule``
     description: str
+    guidance: float = 0.0       # guidance weight w of guided steps (0: no guided steps)
+    guidance_interval: tuple = (0.5, 1.0)   # steps whose start time lies here are guided
 
 
 TINY = ModelConfig(grid=8, width=128, depth=2, heads=4, cond_tokens=64, cond_width=128, dtype="f32")
@@ -88,6 +90,10 @@ WORKLOADS: Dict[str, Workload] = {
     "trellis32_cached": Workload("trellis32_cached", TRELLIS32, 1, 25, 3.0, "fixed70",
                                  "32^3 grid, width 1024, 12 blocks, 1374x1024 cond, bf16, "
                                  "5 full steps then a fixed 70% quota"),
+    "trellis16_cached_cfg": Workload("trellis16_cached_cfg", TRELLIS16, 1, 25, 3.0, "logistic80",
+                                     "trellis16_cached with classifier-free guidance (w = 3, zero "
+                                     "unconditional input) on the steps starting at t in [0.5, 1] "
+                                     "(steps 1-19 under the eta = 3 shift)", guidance=3.0),
 }
 
 
@@ -154,6 +160,11 @@ def make_cond(cfg: ModelConfig, batch: int, seed_base: int = 2000) -> np.ndarray
         rng = np.random.Generator(np.random.PCG64(seed_base + b))
         c[b] = rng.standard_normal((cfg.cond_tokens, cfg.cond_width), dtype=np.float32)
     return round_bf16(c) if cfg.dtype == "bf16" else c
+
+
+def make_uncond(cfg: ModelConfig, batch: int) -> np.ndarray:
+    """Unconditional input of guided steps: all-zero condition tokens, float32 [B][Nc][dc]."""
+    return np.zeros((batch, cfg.cond_tokens, cfg.cond_width), np.float32)
 
 
 def quota_schedule(w: Workload, seed: int = 3000) -> np.ndarray:

@@ -2,6 +2,7 @@
 from __future__ import annotations
 
 import sys
+from typing import Optional
 
 import numpy as np
 
@@ -55,7 +56,10 @@ def depth_variant(cfg: synth.ModelConfig, depth: int) -> synth.ModelConfig:
 class Pair:
     """One model on both sides: the HIP library (through the C ABI) and the oracle."""
 
-    def __init__(self, cfg: synth.ModelConfig, batch: int, seed: int = 0, scale: float = 0.02):
+    def __init__(self, cfg: synth.ModelConfig, batch: int, seed: int = 0, scale: float = 0.02,
+                 uncond: Optional[np.ndarray] = None):
+        """uncond: the unconditional input of guided steps ([B][Nc][dc]); the
+        state is then created for guided steps."""
         import torch
         from paper_2511_22533_amd import f3c
         self.cfg, self.B = cfg, batch
@@ -63,14 +67,21 @@ class Pair:
         self.cond = synth.make_cond(cfg, batch)
         self.x_T = synth.make_noise(cfg, batch)
         self.model = f3c.Model(cfg).load(self.W)
-        self.state = f3c.State(self.model, batch)
+        self.state = f3c.State(self.model, batch, guided=uncond is not None)
         self.cond_dev = to_dev(self.cond)
         self.state.set_cond(self.cond_dev)
+        self.uncond = uncond
+        if uncond is not None:
+            self.uncond_dev = to_dev(uncond)
+            self.state.set_uncond(self.uncond_dev)
         self.oracle = dit.Model(cfg, self.W)
         torch.cuda.synchronize()
 
     def velocity(self):
         return sampler.model_velocity(self.oracle, self.cond)
+
+    def velocity_uncond(self):
+        return sampler.model_velocity(self.oracle, self.uncond)
 
 
 def oracle_selection(v_cache: np.ndarray, v_prev: np.ndarray, n_cache, omega=0.7):

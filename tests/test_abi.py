@@ -75,6 +75,33 @@ def test_state_bytes_and_batch_limits(L):
     assert L.f3c_state_bytes(m.h, 65, ctypes.byref(b)) == f3c.F3C_EINVAL
 
 
+def test_guided_state_bytes_and_limits(L):
+    m = f3c.Model(synth.TRELLIS16)
+    plain, guided = ctypes.c_size_t(), ctypes.c_size_t()
+    assert L.f3c_state_bytes_ex(m.h, 2, 0, ctypes.byref(plain)) == 0
+    assert L.f3c_state_bytes_ex(m.h, 2, f3c.F3C_STATE_GUIDED, ctypes.byref(guided)) == 0
+    legacy = ctypes.c_size_t()
+    assert L.f3c_state_bytes(m.h, 2, ctypes.byref(legacy)) == 0 and legacy.value == plain.value
+    # activations and condition K/V double; caches and selection buffers do not
+    assert plain.value < guided.value < 2 * plain.value
+    assert L.f3c_state_bytes_ex(m.h, 32, f3c.F3C_STATE_GUIDED, ctypes.byref(guided)) == 0
+    assert L.f3c_state_bytes_ex(m.h, 33, f3c.F3C_STATE_GUIDED, ctypes.byref(guided)) == f3c.F3C_EINVAL
+    assert b"guided" in L.f3c_last_error()
+    assert L.f3c_state_bytes_ex(m.h, 1, 6, ctypes.byref(guided)) == f3c.F3C_EINVAL
+    assert L.f3c_guided_step(None, None, 1.0, 0.5, None, 3.0, None) == f3c.F3C_EINVAL
+    assert L.f3c_set_uncond(None, None, None) == f3c.F3C_EINVAL
+
+
+def test_guidance_interval_matches_oracle():
+    from oracle import schedule as osched
+    for eta in (1.0, 2.0, 3.0):
+        for t in f3c.time_grid(25, eta):
+            for lo, hi in ((0.5, 1.0), (0.0, 1.0), (0.25, 0.75)):
+                assert f3c.guidance_active(t, lo, hi) == osched.cfg_active(t, lo, hi)
+    for t in (0.5, 1.0, np.nextafter(0.5, 0.0), 0.0):
+        assert f3c.guidance_active(t) == osched.cfg_active(t)
+
+
 def test_steps_need_loaded_weights_and_valid_quota(L):
     # state creation needs device memory; the checks below fail before touching it
     assert L.f3c_full_step(None, None, 1.0, 0.5, None) == f3c.F3C_EINVAL

@@ -23,13 +23,15 @@ pytestmark = pytest.mark.gpu
 F32 = np.float32
 
 
-def _gpu_step(torch, pair, x_dev, t, tn, n_cache):
+def _gpu_step(torch, pair, x_dev, t, tn, n_cache, w=None):
     before = pair.state.tensors()
     torch.cuda.synchronize()
     vc = before["v_cache"].cpu().numpy()
     vp = before["v_prev"].cpu().numpy()
     x_before = x_dev.cpu().numpy()
-    if any(n_cache):
+    if w is not None:
+        pair.state.guided_step(x_dev, t, tn, n_cache if any(n_cache) else None, w)
+    elif any(n_cache):
         pair.state.cached_step(x_dev, t, tn, n_cache)
     else:
         pair.state.full_step(x_dev, t, tn)
@@ -67,6 +69,39 @@ def _check_step(pair, r, t, tn, n_cache, vel_tol, omega=0.7):
             err = max_rel(r["vact"][lo:hi], want)
             worst = max(worst, err)
             assert err < vel_tol, f"sample {b}: velocity max-rel {err}"
+    return worst
+
+
+def _check_guided_step(pair, r, t, tn, n_cache, w, vel_tol, omega=0.7):
+    """A guided step: selection bit-exact on the guided caches; each pass's
+    velocities against the oracle transformer with its own condition; the
+    guided merge bit-exact given the two passes; cached rows, rotation and
+    Euler bit-exact."""
+    B, N = pair.B, pair.cfg.tokens
+    ref = oracle_selection(r["vc"], r["vp"], n_cache, omega)
+    dt = F32(t - tn)
+    rows = r["off"][-1]
+    assert r["vact"].shape[0] == 2 * rows
+    v_c, v_u = r["vact"][:rows], r["vact"][rows:]
+    guided = sampler.guide(v_c, v_u, w)
+    worst = 0.0
+    for b in range(B):
+        active = ref[b][1]
+        lo, hi = r["off"][b], r["off"][b + 1]
+        assert hi - lo == N - n_cache[b]
+        if any(n_cache):
+            assert np.array_equal(r["idx"][lo:hi], active), f"selection sample {b}"
+        cached = np.setdiff1d(np.arange(N), active)
+        assert np.array_equal(r["vnew"][b][cached].view(np.uint32), r["vc"][b][cached].view(np.uint32))
+        assert np.array_equal(r["vnew"][b][active].view(np.uint32), guided[lo:hi].view(np.uint32)), f"guide {b}"
+        assert np.array_equal(r["vold"][b].view(np.uint32), r["vc"][b].view(np.uint32))
+        assert np.array_equal(r["x1"][b].view(np.uint32), (r["x0"][b] - dt * r["vnew"][b]).view(np.uint32))
+        if hi > lo:
+            for got, c in ((v_c[lo:hi], pair.cond[b]), (v_u[lo:hi], pair.uncond[b])):
+                want = pair.oracle.forward(r["x0"][b][active], active, t, c)
+                err = max_rel(got, want)
+                worst = max(worst, err)
+                assert err < vel_tol, f"sample {b}: velocity max-rel {err}"
     return worst
 
 
@@ -259,3 +294,115 @@ def test_profiler_times_kernels_and_leaves_results_unchanged(torch):
             total = sum(prof[c]["ms"] for c in PROF_CLASSES)
             assert total <= e0.elapsed_time(e1) * 1.02 + 0.01
     assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
+
+
+def _uncond(cfg, batch, seed=2500):
+    """An unconditional input distinct from the condition: seeded N(0, 1) tokens, or zeros (seed None)."""
+    if seed is None:
+        return np.zeros((batch, cfg.cond_tokens, cfg.cond_width), F32)
+    return synth.make_cond(cfg, batch, seed_base=seed)
+
+
+def test_guided_tiny_f32_trajectory(torch):
+    """Guided steps inside the guidance interval, then plain steps, against the
+    oracle step by step and over the trajectory."""
+    w_ = synth.WORKLOADS["tiny_f32"]
+    pair = Pair(w_.model, 2, uncond=_uncond(w_.model, 2))
+    times = schedule.time_grid(w_.steps, w_.shift)
+    quotas = np.concatenate([synth.quota_schedule(w_)] * 2, axis=1)
+    quotas[:, 1] = quotas[:, 1] // 2
+    guided = schedule.guided_steps(times)
+    assert guided[0] and not guided[-1]
+    w = 3.0
+    x = to_dev(pair.x_T)
+    for k in range(w_.steps):
+        q = quotas[k].tolist()
+        say("guided tiny step", k + 1, q, guided[k])
+        if guided[k]:
+            r = _gpu_step(torch, pair, x, times[k], times[k + 1], q, w)
+            _check_guided_step(pair, r, times[k], times[k + 1], q, w, 1e-4)
+        else:
+            r = _gpu_step(torch, pair, x, times[k], times[k + 1], q)
+            _check_step(pair, r, times[k], times[k + 1], q, 1e-4)
+    ref = sampler.sample(pair.x_T, pair.velocity(), times, quotas, uncond=pair.velocity_uncond(), w=w,
+                         guided=guided)
+    assert rel_l2(x.cpu().numpy(), ref.x) < 1e-4
+
+
+def test_guided_passes_are_independent(torch):
+    """With the unconditional input equal to the condition, the two passes get
+    identical rows and identical keys/values, so their outputs must be equal
+    bit for bit (any mixing of the two halves' segments or keys/values breaks
+    it), and the step stays within tolerance of the oracle."""
+    cfg = depth_variant(synth.TRELLIS16, 2)
+    base = Pair(cfg, 2)
+    pair = Pair(cfg, 2, uncond=base.cond.copy())
+    rng = np.random.default_rng(11)
+    vc = (0.5 * rng.standard_normal((2, cfg.tokens, 8))).astype(F32)
+    vp = (vc + 0.05 * rng.standard_normal(vc.shape)).astype(F32)
+    pair.state.import_(np.concatenate([vc.ravel(), vp.ravel()]))
+    x = to_dev(pair.x_T)
+    q = [1500, 3000]
+    say("guided equal passes", q)
+    r = _gpu_step(torch, pair, x, 0.8, 0.75, q, 2.0)
+    rows = r["off"][-1]
+    assert np.array_equal(r["vact"][:rows].view(np.uint32), r["vact"][rows:].view(np.uint32))
+    _check_guided_step(pair, r, 0.8, 0.75, q, 2.0, 2e-2)
+
+
+def test_guided_trellis16_full_depth(torch):
+    """Full-size model, a guided Phase 2 step (50% cached) with a zero unconditional input."""
+    cfg = synth.TRELLIS16
+    pair = Pair(cfg, 1, uncond=_uncond(cfg, 1, seed=None))
+    rng = np.random.default_rng(12)
+    vc = (0.5 * rng.standard_normal((1, cfg.tokens, 8))).astype(F32)
+    vp = (vc + 0.05 * rng.standard_normal(vc.shape)).astype(F32)
+    pair.state.import_(np.concatenate([vc.ravel(), vp.ravel()]))
+    x = to_dev(pair.x_T)
+    t = schedule.time_grid(25, 3.0)
+    say("trellis16 guided step k=12")
+    r = _gpu_step(torch, pair, x, t[11], t[12], [2048], 7.5)
+    err = _check_guided_step(pair, r, t[11], t[12], [2048], 7.5, 2e-2)
+    say("trellis16 guided max-rel", err)
+
+
+def test_guided_batch4_ragged_and_full(torch):
+    cfg = depth_variant(synth.TRELLIS16, 1)
+    pair = Pair(cfg, 4, uncond=_uncond(cfg, 4))
+    x = to_dev(pair.x_T)
+    say("guided b4 full")
+    r = _gpu_step(torch, pair, x, 1.0, 0.98, [0, 0, 0, 0], 1.5)
+    _check_guided_step(pair, r, 1.0, 0.98, [0, 0, 0, 0], 1.5, 2e-2)
+    say("guided b4 ragged")
+    q = [4096, 100, 2500, 3900]                # an empty active set, and ragged ones
+    r = _gpu_step(torch, pair, x, 0.98, 0.95, q, 1.5)
+    _check_guided_step(pair, r, 0.98, 0.95, q, 1.5, 2e-2)
+
+
+def test_guided_step_preconditions(torch):
+    from paper_2511_22533_amd import f3c
+    cfg = synth.TINY
+    plain = Pair(cfg, 1)
+    x = to_dev(plain.x_T)
+    with pytest.raises(f3c.F3CError) as e:
+        plain.state.guided_step(x, 1.0, 0.9, None, 2.0)
+    assert e.value.code == f3c.F3C_ESTATE
+    with pytest.raises(f3c.F3CError) as e:
+        plain.state.set_uncond(plain.cond_dev)
+    assert e.value.code == f3c.F3C_ESTATE
+    g = f3c.State(plain.model, 1, guided=True)
+    g.set_cond(plain.cond_dev)
+    with pytest.raises(f3c.F3CError) as e:             # unconditional input not set
+        g.guided_step(x, 1.0, 0.9, None, 2.0)
+    assert e.value.code == f3c.F3C_ESTATE
+    g.set_uncond(plain.cond_dev)
+    with pytest.raises(f3c.F3CError) as e:
+        g.guided_step(x, 1.0, 0.9, None, float("nan"))
+    assert e.value.code == f3c.F3C_EINVAL
+    # a guided state runs plain steps too, bit-identical to a plain state's
+    x2 = to_dev(plain.x_T)
+    plain.state.cached_step(x, 1.0, 0.9, [0])
+    g.cached_step(x2, 1.0, 0.9, [0])
+    torch.cuda.synchronize()
+    assert torch.equal(x, x2)
+
