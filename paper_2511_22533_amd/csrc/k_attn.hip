@@ -85,6 +85,11 @@ __device__ __forceinline__ float max16(const f32x16& v) {
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 constexpr float kRescaleLog2 = 8.0f;
+// DMA path: a tile's probabilities are taken against the running reference
+// max; when a lane's 32 probabilities sum to more than this, the reference is
+// moved to the tile's max and the tile recomputed (so every probability that
+// enters the PV product is at most 2^16).
+constexpr float kTileSumLimit = 65536.0f;
 
 struct AttnArgs {
   Segs qs, ks;
@@ -115,7 +120,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
   // transpose read. Other types and head sizes stage through registers, with
   // V transposed on its way into LDS.
   constexpr bool DMA = ES == 2 && HD == 64;
-  constexpr int NBUF = DMA ? 4 : 2;
+  constexpr int NBUF = DMA ? 5 : 2;
   constexpr int KRS = DMA ? HD * ES : HD * ES + 16;   // K tile row stride (bytes)
   constexpr int VRS = kBKV * ES + 8;                 // V^T tile row stride (bytes), register path
   constexpr int NKS = HD * ES / 32;          // 32-byte K slices over the head dim
@@ -376,12 +381,127 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
   };
 
   if constexpr (DMA) {
-    // Four buffers, tile t in buffer (t - t_begin) % 4, loads three tiles
-    // ahead. Step t waits for tile t + 1 (tile t + 2 stays in flight); the
-    // barrier makes every wave's DMA visible and retires buffer (t - 1) % 4,
-    // which receives tile t + 3 (clamped: past the end the last tile is
-    // re-read). Then the scores of tile t + 1 are issued to the matrix cores
-    // before the softmax of tile t, so that VALU work overlaps them.
+    // Five buffers, tile t in buffer (t - t_begin) % 5, loads three tiles
+    // ahead. Iteration t waits for tile t + 1 (tile t + 2 stays in flight);
+    // its barrier makes every wave's DMA visible and retires the buffer of
+    // tile t - 2 (last read by the PV product of iteration t - 1), which
+    // receives tile t + 3 (clamped: past the end the last tile is re-read).
+    // The matrix cores then take the scores of tile t + 1 and the PV product
+    // of tile t - 1 while the vector unit computes the probabilities of tile
+    // t: the three are independent, so the steady-state iteration is one
+    // basic block the scheduler can interleave. The first and last tiles are
+    // peeled. Probabilities use a reference max that moves only in the rare
+    // fix-up branch (kTileSumLimit), so no per-tile max is computed.
+    const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
+    auto qk2 = [&](int buf, f32x16 (&s)[2]) {
+      const char* Ks = lds + buf * (KBUF + VBUF);
+      u32x4 kf[2][NKS];
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int q = 0; q < NKS; ++q)
+          kf[kt][q] = *reinterpret_cast<const u32x4*>(Ks + (kt * 32 + r32) * KRS + (((2 * q + g) ^ kswz) << 4));
+#pragma unroll
+      for (int q = 0; q < NKS; ++q)
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+          s[kt] = Mfma<T>::mma(__builtin_bit_cast(bf16x8, kf[kt][q]), __builtin_bit_cast(bf16x8, qf[q]),
+                               q == 0 ? f32x16{} : s[kt]);
+    };
+    // O^T += V^T P^T for the tile in buffer buf; keys kb..kb+3 and kb+8..kb+11
+    // at column h*32 + (lane%32) through two transpose reads of the row-major
+    // V tile (the K-slot order of P).
+    auto pv2 = [&](int buf, const bf16x8 (&pf)[2][2]) {
+      const char* Vt = lds + buf * (KBUF + VBUF) + KBUF;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int h = 0; h < HT; ++h) {
+            const int kb = kt * 32 + 16 * u + 4 * g, col = h * 32 + vcol;
+            const char* a0 = Vt + (kb + vrow) * (HD * ES) + (((col >> 3) ^ vswz) << 4) + (col & 7) * ES;
+            const auto lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)a0);
+            const auto hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(a0 + 8 * HD * ES));
+            const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+            oacc[h] = Mfma<T>::mma(vf, pf[kt][u], oacc[h]);
+          }
+    };
+    // Keys of element e: kv0 + 32*kt + 8*(e/4) + 4*g + e%4; mask those past nk.
+    auto mask2 = [&](int t, f32x16 (&s)[2]) {
+      const int kv0 = t * kBKV;
+      if (kv0 + kBKV > nk) {
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            if (kv0 + kt * 32 + 8 * (e >> 2) + 4 * g + (e & 3) >= nk) s[kt][e] = -INFINITY;
+      }
+    };
+    // Probabilities 2^((s - m_run) c) as the bf16 P fragments; returns their
+    // sum as rounded for the PV product (v_dot2 with ones).
+    auto probs = [&](const f32x16 (&s)[2], bf16x8 (&pf)[2][2]) {
+      const float mc = m_run * c;
+      float part[4];                     // four independent accumulation chains
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) pf[kt][u][e] = (bf16)__builtin_amdgcn_exp2f(fmaf(s[kt][8 * u + e], c, -mc));
+          const bf16x8& f = pf[kt][u];
+          float a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(f, f, 0, 1), ones, 0.0f, false);
+          a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(f, f, 2, 3), ones, a, false);
+          a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(f, f, 4, 5), ones, a, false);
+          part[2 * kt + u] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(f, f, 6, 7), ones, a, false);
+        }
+      return (part[0] + part[1]) + (part[2] + part[3]);
+    };
+    // The query's max over this tile (both key halves of the wave).
+    auto tile_max = [&](const f32x16 (&s)[2]) {
+      const float m0 = max16(s[0]), m1 = max16(s[1]);
+      const float mx = max3(m0, m1, m1);
+      return fmaxf(mx, __shfl_xor(mx, 32));
+    };
+    // Rare: some lane's probabilities outgrew the reference; move it to the
+    // tile's max, rescale what was accumulated (including the PV product of
+    // the previous tile, issued before) and redo the tile.
+    auto fixup = [&](const f32x16 (&s)[2], bf16x8 (&pf)[2][2], float& lt) {
+      if (__builtin_amdgcn_ballot_w64(lt > kTileSumLimit) != 0) {
+        const float m_new = fmaxf(m_run, tile_max(s));
+        const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c);
+        m_run = m_new;
+        l_run *= alpha;
+#pragma unroll
+        for (int u = 0; u < HT; ++u)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) oacc[u][e] *= alpha;
+        lt = probs(s, pf);
+      }
+    };
+    auto bnext = [](int b, int k) { b += k; return b >= 5 ? b - 5 : b; };
+    // Iteration t with S(t) in cur and P(t-1) in pprev: S(t+1) -> next, P(t) -> pcur.
+    auto mid = [&](int t, int buf, f32x16 (&cur)[2], f32x16 (&next)[2], const bf16x8 (&pprev)[2][2],
+                   bf16x8 (&pcur)[2][2], auto first) {
+      wait_vm(std::integral_constant<int, 2 * DQ>{});
+      __syncthreads();
+      fetch_dma(min((t + 3) * kBKV, last_kv), bnext(buf, 3));
+      qk2(bnext(buf, 1), next);
+      if constexpr (!decltype(first)::value) pv2(bnext(buf, 4), pprev);
+      float lt = probs(cur, pcur);
+      fixup(cur, pcur, lt);
+      l_run += lt;
+    };
+    // Last tile t (maybe ragged): PV(t-1), P(t), then PV(t).
+    auto last = [&](int t, int buf, f32x16 (&cur)[2], const bf16x8 (&pprev)[2][2], bf16x8 (&pcur)[2][2],
+                    auto first) {
+      if constexpr (!decltype(first)::value) pv2(bnext(buf, 4), pprev);
+      mask2(t, cur);
+      float lt = probs(cur, pcur);
+      fixup(cur, pcur, lt);
+      l_run += lt;
+      pv2(buf, pcur);
+    };
     if (t_begin < t_end) {               // uniform over the workgroup
       // Q first: otherwise the compiler, which does not see the DMA, keeps its
       // wait for the Q fragments inside the loop as a full vmcnt(0).
@@ -393,20 +513,28 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
       wait_vm(std::integral_constant<int, 4 * DQ>{});
       __syncthreads();
       f32x16 sa[2], sb[2];
-      qk(0, sa);
-      auto step = [&](int t, int buf, f32x16 (&cur)[2], f32x16 (&next)[2]) {
-        wait_vm(std::integral_constant<int, 2 * DQ>{});
-        __syncthreads();
-        fetch_dma(min((t + 3) * kBKV, last_kv), (buf + 3) & 3);
-        if (t + 1 < t_end) qk((buf + 1) & 3, next);
-        softmax_pv(t, buf, cur);
-      };
-      int t = t_begin, buf = 0;
-      for (; t + 1 < t_end; t += 2, buf = (buf + 2) & 3) {
-        step(t, buf, sa, sb);
-        step(t + 1, (buf + 1) & 3, sb, sa);
+      bf16x8 pa[2][2], pb[2][2];
+      qk2(0, sa);
+      if (t_begin + 1 == t_end) mask2(t_begin, sa);
+      m_run = tile_max(sa);              // reference max: the first tile's
+      const std::true_type yes{};
+      const std::false_type no{};
+      if (t_begin + 1 == t_end) {
+        last(t_begin, 0, sa, pb, pa, yes);
+      } else {
+        mid(t_begin, 0, sa, sb, pb, pa, yes);          // S(t+1) in sb, P(t) in pa
+        int t = t_begin + 1, buf = 1;
+        for (; t + 2 < t_end; t += 2, buf = bnext(buf, 2)) {
+          mid(t, buf, sb, sa, pa, pb, no);
+          mid(t + 1, bnext(buf, 1), sa, sb, pb, pa, no);
+        }
+        if (t + 1 < t_end) {
+          mid(t, buf, sb, sa, pa, pb, no);
+          last(t + 1, bnext(buf, 1), sa, pb, pa, no);
+        } else {
+          last(t, buf, sb, pa, pb, no);
+        }
       }
-      if (t < t_end) step(t, buf, sa, sb);
       // no DMA may still target this workgroup's LDS when it retires
       wait_vm(std::integral_constant<int, 0>{});
     }

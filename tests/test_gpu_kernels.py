@@ -158,7 +158,10 @@ def test_gemm_f32(torch, M, N, K, epi):
     assert max_rel(got, want) < 1e-5
 
 
-def _attn_case(torch, dt, heads, hd, q_lens, k_lens, seed, sample_queries=None, workspace=False, outputs=None):
+def _attn_case(torch, dt, heads, hd, q_lens, k_lens, seed, sample_queries=None, workspace=False, outputs=None,
+               key_ramp=0.0):
+    """key_ramp > 0 scales key j of each sample by 1 + key_ramp * (j // 64): every
+    64-key tile then has larger scores than the ones before it."""
     from paper_2511_22533_amd import f3c
     rng = np.random.default_rng(seed)
     d = heads * hd
@@ -167,6 +170,9 @@ def _attn_case(torch, dt, heads, hd, q_lens, k_lens, seed, sample_queries=None, 
     q = (1.5 * rng.standard_normal((q_off[-1], d))).astype(np.float32)
     k = (1.5 * rng.standard_normal((k_off[-1], d))).astype(np.float32)
     v = rng.standard_normal((k_off[-1], d)).astype(np.float32)
+    if key_ramp:
+        j = np.concatenate([np.arange(n) for n in k_lens]) if k_off[-1] else np.zeros(0, int)
+        k *= (1.0 + key_ramp * (j // 64)).astype(np.float32)[:, None]
     tdt = torch.bfloat16 if dt == f3c.F3C_BF16 else torch.float32
     if dt == f3c.F3C_BF16:
         q, k, v = bf16_round(q), bf16_round(k), bf16_round(v)
@@ -225,6 +231,19 @@ def test_attention_bf16_split_keys(torch, q_lens, k_lens):
         assert _attn_case(torch, f3c.F3C_BF16, 16, 64, q_lens, k_lens, seed=sum(k_lens), workspace=True,
                           outputs=outs) < 2e-2
     assert np.array_equal(outs[0], outs[1])
+
+
+# Scores that grow from tile to tile: the running reference max of the
+# matrix-core path is too small for later tiles, so its fix-up branch
+# (rescale what was accumulated, redo the tile) runs, for some queries of a
+# wave and not others; in the four-wave, eight-wave and key-split launches.
+@pytest.mark.parametrize("q_lens,k_lens,ramp,ws", [([300], [300], 2.0, False), ([1000], [1000], 0.5, False),
+                                                   ([820], [1374], 1.0, False), ([300], [1374], 2.0, True),
+                                                   ([37, 3000], [37, 3000], 0.3, False), ([640], [640], 0.12, False)])
+def test_attention_bf16_growing_scores(torch, q_lens, k_lens, ramp, ws):
+    from paper_2511_22533_amd import f3c
+    assert _attn_case(torch, f3c.F3C_BF16, 16, 64, q_lens, k_lens, seed=int(10 * ramp) + len(q_lens),
+                      workspace=ws, key_ramp=ramp, sample_queries=128) < 2e-2
 
 
 @pytest.mark.parametrize("hd,heads", [(32, 4), (64, 2)])
