@@ -224,12 +224,11 @@ int f3c_op_select(int32_t batch, int32_t n_tokens, const float* v_cache, const f
  * epilogue 0: out T [M][ldo] = value; 1: out = GELU_tanh(value);
  * 2: resid f32 [M][ldr] += (gate ? gate[n] : 1) * value.
  * Requires N % 128 == 0, K a multiple of 64 (bf16) / 32 (f32), 16-byte aligned
- * rows, ldo and ldr multiples of 4. workspace (device, may be NULL) lets
- * small-M long-K shapes split along K; the split sums are reduced in a fixed
- * order, so results do not depend on scheduling. */
+ * rows, ldo and ldr multiples of 4. Every output is one workgroup's sum in a
+ * fixed order, so results do not depend on scheduling. */
 int f3c_op_gemm(int32_t dtype, int32_t epilogue, int32_t M, int32_t N, int32_t K, const void* A, int32_t lda,
                 const void* W, int32_t ldw, const float* bias, const float* gate, void* out, int32_t ldo,
-                float* resid, int32_t ldr, float* workspace, size_t workspace_bytes, f3c_stream stream);
+                float* resid, int32_t ldr, f3c_stream stream);
 
 /* Varlen multi-head attention: sample b's queries are rows q_off[b]..q_off[b+1]
  * of q (T, row stride ldq), its keys/values rows k_off[b]..k_off[b+1] of k/v;

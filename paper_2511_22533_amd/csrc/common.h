@@ -98,6 +98,28 @@ __device__ __forceinline__ int xcd_logical_id(int hw, int total) {
   return x * q + (x < r ? x : r) + i;
 }
 
+// 16 bytes per lane from global memory straight into LDS at lds_block + 16 *
+// lane (gfx950 global_load_lds_dwordx4; the block base is wave-uniform and
+// goes through M0). Written as inline assembly so that the compiler does not
+// track it: it would otherwise wait for every outstanding LDS load of this
+// kind before any LDS read. A kernel using it orders these loads itself (an
+// s_waitcnt on the vector-memory counter and a barrier before a tile is
+// read); waits the compiler places for its own loads only grow more
+// conservative, since the counter retires in issue order.
+__device__ __forceinline__ void dma16(const char* gptr, char* lds_block) {
+  const uint32_t base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_block;
+  asm volatile("global_load_lds_dwordx4 %0, off" : : "v"(gptr), "{m0}"(__builtin_amdgcn_readfirstlane(base))
+               : "memory");
+}
+
+// Wait until at most N vector-memory operations are outstanding (gfx9
+// s_waitcnt encoding; expcnt and lgkmcnt left at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
 // Sample lookup in a segment table off[0..B] (off[B] = total rows).
 __device__ __forceinline__ int find_segment(const int* off, int B, int row) {
   int b = 0;

@@ -40,7 +40,11 @@ int fail(int code, const char* fmt, ...) {
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-constexpr size_t kSplitWsBytes = size_t(32) << 20;   // split-K workspace per state
+// Attention key-split partials per state. A launch splits only while its
+// 128-query tiles x heads x splits stay within 256 workgroups, so the partials
+// never exceed 256 x 128 rows of head_dim + 2 floats (8.25 MiB at 64); with
+// less room the launch uses fewer splits.
+constexpr size_t kAttnWsBytes = size_t(12) << 20;
 
 struct Spec {
   std::string name;
@@ -87,7 +91,7 @@ struct f3c_state {
   float *h, *vact, *mod, *temb, *score;
   void *u, *qkv, *att, *qc, *hid, *cond_t, *kv;
   int32_t *idx, *pos;
-  float* ws = nullptr;          // split-K partial sums
+  float* ws = nullptr;          // attention key-split partials
   size_t ws_bytes = 0;
   bool guided = false;          // activations and condition K/V sized for two passes per sample
   bool cond_set = false, uncond_set = false, record_scores = false;
@@ -267,7 +271,7 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
       {
         Scope sc(s, F3C_PROF_GEMM_QKV, st, 2.0 * rows * 3 * d * d, proj_bytes(3 * dd, dd, false));
         HIP_TRY(launch_gemm(SITE_QKV, dt, EPI_STORE, rows, 3 * d, d, s->u, d, m->w(p + "qkv_w"), d, m->b(p + "qkv_b"),
-                            nullptr, s->qkv, 3 * d, nullptr, 0, s->ws, s->ws_bytes, st));
+                            nullptr, s->qkv, 3 * d, nullptr, 0, st));
       }
       {
         double fl = 0;
@@ -281,7 +285,7 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
       {
         Scope sc(s, F3C_PROF_GEMM_O, st, 2.0 * rows * d * d, proj_bytes(dd, dd, true));
         HIP_TRY(launch_gemm(SITE_O, dt, EPI_RESID, rows, d, d, s->att, d, m->w(p + "o_w"), d, m->b(p + "o_b"), md + 2 * d,
-                            nullptr, 0, s->h, d, s->ws, s->ws_bytes, st));
+                            nullptr, 0, s->h, d, st));
       }
       {
         Scope sc(s, F3C_PROF_LN, st, 0, lnb);
@@ -290,7 +294,7 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
       {
         Scope sc(s, F3C_PROF_GEMM_Q, st, 2.0 * rows * d * d, proj_bytes(dd, dd, false));
         HIP_TRY(launch_gemm(SITE_Q, dt, EPI_STORE, rows, d, d, s->u, d, m->w(p + "q_w"), d, m->b(p + "q_b"), nullptr,
-                            s->qc, d, nullptr, 0, s->ws, s->ws_bytes, st));
+                            s->qc, d, nullptr, 0, st));
       }
       {
         Scope sc(s, F3C_PROF_ATTN_CROSS, st, 4.0 * rows * m->Nc * d, (2.0 * r + 2.0 * cond_rows) * dd * E);
@@ -301,7 +305,7 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
       {
         Scope sc(s, F3C_PROF_GEMM_CO, st, 2.0 * rows * d * d, proj_bytes(dd, dd, true));
         HIP_TRY(launch_gemm(SITE_CO, dt, EPI_RESID, rows, d, d, s->att, d, m->w(p + "co_w"), d, m->b(p + "co_b"), nullptr,
-                            nullptr, 0, s->h, d, s->ws, s->ws_bytes, st));
+                            nullptr, 0, s->h, d, st));
       }
       {
         Scope sc(s, F3C_PROF_LN, st, 0, lnb);
@@ -310,12 +314,12 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
       {
         Scope sc(s, F3C_PROF_GEMM_FC1, st, 2.0 * rows * dm * d, proj_bytes(dm, dd, false));
         HIP_TRY(launch_gemm(SITE_FC1, dt, EPI_GELU, rows, dm, d, s->u, d, m->w(p + "fc1_w"), d, m->b(p + "fc1_b"), nullptr,
-                            s->hid, dm, nullptr, 0, s->ws, s->ws_bytes, st));
+                            s->hid, dm, nullptr, 0, st));
       }
       {
         Scope sc(s, F3C_PROF_GEMM_FC2, st, 2.0 * rows * d * dm, proj_bytes(dd, dm, true));
         HIP_TRY(launch_gemm(SITE_FC2, dt, EPI_RESID, rows, d, dm, s->hid, dm, m->w(p + "fc2_w"), dm, m->b(p + "fc2_b"),
-                            md + 5 * d, nullptr, 0, s->h, d, s->ws, s->ws_bytes, st));
+                            md + 5 * d, nullptr, 0, s->h, d, st));
       }
     }
     {
@@ -509,7 +513,7 @@ int f3c_state_bytes_ex(const f3c_model* m, int32_t batch, uint32_t flags, size_t
   t += align256(2 * d * 4);                    // temb scratch
   t += align256((size_t)P * batch * m->Nc * m->dc * es);            // condition tokens
   t += align256((size_t)P * batch * m->Nc * 2 * m->L * d * es);     // cross K/V, all blocks
-  t += kSplitWsBytes;                                                 // split-K partials
+  t += kAttnWsBytes;                                                  // attention split partials
   *bytes = t;
   return F3C_OK;
 }
@@ -551,8 +555,8 @@ int f3c_state_create_ex(f3c_model* m, int32_t batch, uint32_t flags, void* state
   s->temb = (float*)take(2 * d * 4);
   s->cond_t = take(P * batch * m->Nc * m->dc * es);
   s->kv = take(P * batch * m->Nc * 2 * m->L * d * es);
-  s->ws = (float*)take(kSplitWsBytes);
-  s->ws_bytes = kSplitWsBytes;
+  s->ws = (float*)take(kAttnWsBytes);
+  s->ws_bytes = kAttnWsBytes;
   hipStream_t st = (hipStream_t)stream;
   hipError_t e = hipMemsetAsync(s->v[0], 0, R * 32, st);
   if (e == hipSuccess) e = hipMemsetAsync(s->v[1], 0, R * 32, st);
@@ -605,7 +609,7 @@ int cond_kv(f3c_state* s, const float* cond_dev, int half, hipStream_t st) {
   Scope sc(s, F3C_PROF_COND, st, 2.0 * rows * n * m->dc, 0);
   HIP_TRY(launch_convert(m->cfg.dtype, cond_dev, ct, (int64_t)rows * m->dc, st));
   HIP_TRY(launch_gemm(SITE_COND, m->cfg.dtype, EPI_STORE, rows, n, m->dc, ct, m->dc, m->wdev + m->kv_w, m->dc,
-                      (const float*)(m->wdev + m->kv_b), nullptr, kv, n, nullptr, 0, s->ws, s->ws_bytes, st));
+                      (const float*)(m->wdev + m->kv_b), nullptr, kv, n, nullptr, 0, st));
   return F3C_OK;
 }
 
@@ -769,7 +773,7 @@ int f3c_op_select(int32_t batch, int32_t n_tokens, const float* v_cache, const f
 
 int f3c_op_gemm(int32_t dtype, int32_t epilogue, int32_t M, int32_t N, int32_t K, const void* A, int32_t lda,
                 const void* W, int32_t ldw, const float* bias, const float* gate, void* out, int32_t ldo,
-                float* resid, int32_t ldr, float* workspace, size_t workspace_bytes, f3c_stream stream) {
+                float* resid, int32_t ldr, f3c_stream stream) {
   if (dtype != F3C_F32 && dtype != F3C_BF16) return fail(F3C_EINVAL, "bad dtype");
   if (epilogue < 0 || epilogue > 2) return fail(F3C_EINVAL, "bad epilogue");
   const int es = dtype == F3C_BF16 ? 2 : 4;
@@ -780,9 +784,8 @@ int f3c_op_gemm(int32_t dtype, int32_t epilogue, int32_t M, int32_t N, int32_t K
   if (!A || !W || !bias) return fail(F3C_EINVAL, "NULL operand");
   if (epilogue == 2 ? (!resid || ldr < N || ldr % 4) : (!out || ldo < N || ldo % 4))
     return fail(F3C_EINVAL, "bad output (leading dim below N or not a multiple of 4)");
-  if (workspace && ((uintptr_t)workspace & 15)) return fail(F3C_EINVAL, "workspace must be 16-byte aligned");
   HIP_TRY(launch_gemm(SITE_OP, dtype, epilogue, M, N, K, A, lda, W, ldw, bias, gate, out, ldo, resid, ldr,
-                      workspace, workspace ? workspace_bytes : 0, (hipStream_t)stream));
+                      (hipStream_t)stream));
   return F3C_OK;
 }
 

@@ -39,20 +39,6 @@ namespace {
 
 constexpr int kBKV = 64;             // keys per LDS tile
 
-// 16 bytes per lane from global memory straight into LDS at lds_block + 16 *
-// lane (gfx950 global_load_lds_dwordx4; the block base is wave-uniform and
-// goes through M0). Written as inline assembly so that the compiler does not
-// track it: it would otherwise wait for every outstanding LDS load of this
-// kind before any LDS transpose read. The kernel orders these loads itself
-// (an s_waitcnt on the vector-memory counter and a barrier before a tile is
-// read); waits the compiler places for its own loads only grow more
-// conservative, since the counter retires in issue order.
-__device__ __forceinline__ void dma16(const char* gptr, char* lds_block) {
-  const uint32_t base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_block;
-  asm volatile("global_load_lds_dwordx4 %0, off" : : "v"(gptr), "{m0}"(__builtin_amdgcn_readfirstlane(base))
-               : "memory");
-}
-
 // max(a, b, c) as one v_max3_f32. fmaxf on MFMA results costs three
 // instructions each (both inputs are first quieted with v_max x, x, since the
 // compiler cannot prove they are not signalling NaNs); the scores here are
@@ -233,12 +219,6 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
       dma16(p.k + kofs + ((phys ^ ((row >> 1) & 7)) << 4), Ks + blk * 1024);
       dma16(p.v + vofs + ((phys ^ (((row >> 1) & 1) << 2)) << 4), Vs + blk * 1024);
     }
-  };
-  // Wait until at most n vector-memory operations are outstanding (gfx9
-  // s_waitcnt encoding; expcnt and lgkmcnt left at their maxima).
-  auto wait_vm = [](auto n) {
-    constexpr int v = decltype(n)::value;
-    __builtin_amdgcn_s_waitcnt((v & 15) | (7 << 4) | (15 << 8) | ((v >> 4) << 14));
   };
 
   f32x16 oacc[HT];
@@ -483,7 +463,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
     // Iteration t with S(t) in cur and P(t-1) in pprev: S(t+1) -> next, P(t) -> pcur.
     auto mid = [&](int t, int buf, f32x16 (&cur)[2], f32x16 (&next)[2], const bf16x8 (&pprev)[2][2],
                    bf16x8 (&pcur)[2][2], auto first) {
-      wait_vm(std::integral_constant<int, 2 * DQ>{});
+      wait_vm<2 * DQ>();
       __syncthreads();
       fetch_dma(min((t + 3) * kBKV, last_kv), bnext(buf, 3));
       qk2(bnext(buf, 1), next);
@@ -506,11 +486,11 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
       // Q first: otherwise the compiler, which does not see the DMA, keeps its
       // wait for the Q fragments inside the loop as a full vmcnt(0).
       __builtin_amdgcn_sched_barrier(0);
-      wait_vm(std::integral_constant<int, 0>{});
+      wait_vm<0>();
       fetch_dma(t_begin * kBKV, 0);
       fetch_dma(min((t_begin + 1) * kBKV, last_kv), 1);
       fetch_dma(min((t_begin + 2) * kBKV, last_kv), 2);
-      wait_vm(std::integral_constant<int, 4 * DQ>{});
+      wait_vm<4 * DQ>();
       __syncthreads();
       f32x16 sa[2], sb[2];
       bf16x8 pa[2][2], pb[2][2];
@@ -536,7 +516,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
         }
       }
       // no DMA may still target this workgroup's LDS when it retires
-      wait_vm(std::integral_constant<int, 0>{});
+      wait_vm<0>();
     }
   } else {
     // Fetches are unconditional (past the end they re-read the last tile), so

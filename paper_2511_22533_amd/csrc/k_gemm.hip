@@ -93,9 +93,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs p) {
     m0 = y * BM;
   }
   const size_t lda_b = (size_t)p.lda * ES, ldw_b = (size_t)p.ldw * ES;
-  // Split-K: slice z of gridDim.z covers K tiles [z*KT, (z+1)*KT).
-  const int KT = (p.K * ES) / kBKB / (int)gridDim.z;
-  const size_t k_base = (size_t)blockIdx.z * KT * kBKB;
+  const int KT = (p.K * ES) / kBKB;
+  constexpr size_t k_base = 0;
 
   // Rows past M are loaded from row M-1 (always valid) and never stored.
   const char* a_row[CA];
@@ -239,12 +238,6 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs p) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int col = n0 + wn * WTN + j * 32 + 8 * q + 4 * g;
-        if constexpr (EPI == EPI_PARTIAL) {
-          float* part = p.resid + ((size_t)blockIdx.z * p.M + row) * p.N + col;
-          *reinterpret_cast<float4*>(part) =
-              make_float4(acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-          continue;
-        }
         const float4 bv = *reinterpret_cast<const float4*>(p.bias + col);
         float v[4] = {acc[i][j][4 * q] + bv.x, acc[i][j][4 * q + 1] + bv.y, acc[i][j][4 * q + 2] + bv.z,
                       acc[i][j][4 * q + 3] + bv.w};
@@ -269,41 +262,204 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs p) {
   }
 }
 
-// Split-K reduction: value = sum over slices in slice order (deterministic) +
-// bias, then the site's epilogue. One thread per 4 consecutive outputs.
-template <typename T, int EPI, int SITE>
-__global__ __launch_bounds__(256) void k_splitk_reduce(GemmArgs p, const float* __restrict__ part, int splits) {
-  const int64_t i4 = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t total4 = (int64_t)p.M * p.N / 4;
-  if (i4 >= total4) return;
-  const int row = (int)(i4 * 4 / p.N), col = (int)(i4 * 4 % p.N);
-  float4 acc = *reinterpret_cast<const float4*>(part + (size_t)row * p.N + col);
-  for (int z = 1; z < splits; ++z) {
-    const float4 v = *reinterpret_cast<const float4*>(part + ((size_t)z * p.M + row) * p.N + col);
-    acc.x += v.x;
-    acc.y += v.y;
-    acc.z += v.z;
-    acc.w += v.w;
+// bf16 path. Workgroup tile BM x BN; every wave owns a 64 x 64 block (2 x 2
+// accumulators of 32 x 32), so an MFMA costs 1 KiB of LDS reads (the
+// 32 x 64-wave tiles above cost 1.5 KiB, more than the LDS delivers per
+// MFMA). The NW waves are (BM/64)(BN/64) positions times KG K-groups: within
+// every 64-element K tile, group kg takes the 16-element K-steps kg, kg + KG,
+// ..., and at the end the groups' partial blocks are summed through LDS in
+// group order (deterministic); each group then writes 4/KG of the block.
+// K tiles go global -> LDS by DMA (no registers) into four buffers, three
+// tiles ahead, one barrier per tile. LDS rows are the 128 bytes of a row's K
+// tile with their 16-byte chunks XOR-swizzled by (row >> 1) & 7, which makes
+// the fragment reads of 16 consecutive rows conflict-free.
+template <int BM, int BN, int NW, int EPI, int SITE, int KTB = 128, int STAGES = 4, int DIST = 3>
+__global__ __launch_bounds__(64 * NW) void k_gemm2(GemmArgs p) {
+  constexpr int PM = BM / 64, PN = BN / 64, NPOS = PM * PN, KG = NW / NPOS;
+  static_assert(NW % NPOS == 0 && (KG == 1 || KG == 2 || KG == 4), "waves must be positions x 1, 2 or 4");
+  static_assert(KTB == 64 || KTB == 128, "K tile of 32 or 64 elements");
+  static_assert((STAGES & (STAGES - 1)) == 0 && DIST < STAGES, "power-of-two stages, distance below");
+  constexpr int CPR = KTB / 16;                         // 16-byte chunks per row
+  constexpr int KSTEPS = KTB / 32 / KG;
+  static_assert(KSTEPS >= 1, "each K-group needs a K-step per tile");
+  constexpr int ABUF = BM * KTB, SBUF = (BM + BN) * KTB;
+  constexpr int RPB = 1024 / KTB;                       // rows per 1 KiB DMA block
+  constexpr int DA = BM / RPB, DB = BN / RPB;           // 1 KiB DMA blocks of a K tile
+  constexpr int DQ = (DA + DB + NW - 1) / NW;           // blocks per wave
+  constexpr int RED = NPOS * 4 * (KG - 1) * 4096;      // partial blocks exchanged at the end
+  static_assert(RED <= STAGES * SBUF, "reduction must fit in the stage buffers");
+  __shared__ __attribute__((aligned(16))) char lds[STAGES * SBUF];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int pos = wave % NPOS, kg = wave / NPOS;
+  const int wm = pos / PN, wn = pos % PN;
+  const int g = lane >> 5, r32 = lane & 31;
+  int n0, m0;
+  {
+    const int gx = p.N / BN, gy = (p.M + BM - 1) / BM;
+    const int l = xcd_logical_id(blockIdx.x, gx * gy);
+    const int gq = gx / p.xq, per_group = gy * gq;
+    const int grp = l / per_group, r = l - grp * per_group;
+    const int y = r / gq;
+    n0 = (grp * gq + (r - y * gq)) * BN;
+    m0 = y * BM;
   }
-  const float4 bv = *reinterpret_cast<const float4*>(p.bias + col);
-  float v[4] = {acc.x + bv.x, acc.y + bv.y, acc.z + bv.z, acc.w + bv.w};
-  if constexpr (EPI == EPI_RESID) {
-    float4 gv = make_float4(1.0f, 1.0f, 1.0f, 1.0f);
-    if (p.gate) gv = *reinterpret_cast<const float4*>(p.gate + col);
-    float4* r = reinterpret_cast<float4*>(p.resid + (size_t)row * p.ldr + col);
-    float4 h = *r;
-    h.x += gv.x * v[0];
-    h.y += gv.y * v[1];
-    h.z += gv.z * v[2];
-    h.w += gv.w * v[3];
-    *r = h;
-  } else {
-    if constexpr (EPI == EPI_GELU) {
+  const size_t lda_b = (size_t)p.lda * 2, ldw_b = (size_t)p.ldw * 2;
+  const int KT = (p.K * 2) / KTB;
+  constexpr size_t k_base = 0;
+
+  // Swizzle of a row's 16-byte chunks: with 128-byte rows, (row >> 1) & 7;
+  // with 64-byte rows, (row >> 2) & 3. Either way the fragment reads of 16
+  // consecutive rows at one logical chunk hit all 64 banks once.
+  auto swizzle = [](int row) { return KTB == 128 ? (row >> 1) & 7 : (row >> 2) & 3; };
+  // DMA block b: A rows RPB*b.. (b < DA) or W rows RPB*(b - DA)..; lane l
+  // fills row RPB*b + l/CPR at physical chunk l%CPR, i.e. loads the logical
+  // chunk that the row's swizzle maps there. Rows past M re-read row M - 1
+  // (never stored).
+  const char* dsrc[DQ];
+  int doff[DQ];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = gelu_tanh(v[e]);
+  for (int q = 0; q < DQ; ++q) {
+    const int blk = min(wave + NW * q, DA + DB - 1);
+    const int phys = lane % CPR;
+    if (blk < DA) {
+      const int row = RPB * blk + lane / CPR;
+      dsrc[q] = p.A + (size_t)min(m0 + row, p.M - 1) * lda_b + k_base + ((phys ^ swizzle(row)) << 4);
+      doff[q] = blk * 1024;
+    } else {
+      const int row = RPB * (blk - DA) + lane / CPR;
+      dsrc[q] = p.W + (size_t)(n0 + row) * ldw_b + k_base + ((phys ^ swizzle(row)) << 4);
+      doff[q] = ABUF + (blk - DA) * 1024;
     }
-    store4<T>(reinterpret_cast<T*>(p.out) + (size_t)row * p.ldo + col, v);
   }
+  auto fetch = [&](int kt, int buf) {
+#pragma unroll
+    for (int q = 0; q < DQ; ++q) dma16(dsrc[q] + (size_t)kt * KTB, lds + buf * SBUF + doff[q]);
+  };
+
+  // Fragment reads: lane reads 16 bytes of row (block row + 32 i + r32) at
+  // logical chunk 2 ks + g.
+  const int swz = swizzle(r32);
+  int chofs[KSTEPS];
+#pragma unroll
+  for (int s = 0; s < KSTEPS; ++s) chofs[s] = ((2 * (kg + KG * s) + g) ^ swz) << 4;
+  const int a_row = (wm * 64 + r32) * KTB, b_row = ABUF + (wn * 64 + r32) * KTB;
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+
+  auto compute = [&](int buf) {
+    const char* base = lds + buf * SBUF;
+#pragma unroll
+    for (int s = 0; s < KSTEPS; ++s) {
+      u32x4 fa[2], fb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) fa[i] = *reinterpret_cast<const u32x4*>(base + a_row + i * 32 * KTB + chofs[s]);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) fb[j] = *reinterpret_cast<const u32x4*>(base + b_row + j * 32 * KTB + chofs[s]);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = Mfma<bf16>::mma(__builtin_bit_cast(bf16x8, fb[j]), __builtin_bit_cast(bf16x8, fa[i]), acc[i][j]);
+    }
+  };
+
+  // Tile kt in buffer kt % STAGES. Iteration kt waits for tile kt (the next
+  // DIST - 1 tiles stay in flight); the barrier makes every wave's DMA visible
+  // and retires the buffer of tile kt - 1 (or older), which receives tile
+  // kt + DIST (clamped: past the end the last tile is re-read, so the wait
+  // count stays fixed).
+#pragma unroll
+  for (int r = 0; r < DIST; ++r) fetch(min(r, KT - 1), r);
+  int buf = 0;
+  for (int kt = 0; kt < KT; ++kt) {
+    wait_vm<(DIST - 1) * DQ>();
+    __syncthreads();
+    fetch(min(kt + DIST, KT - 1), (buf + DIST) & (STAGES - 1));
+    compute(buf);
+    buf = (buf + 1) & (STAGES - 1);
+  }
+  wait_vm<0>();
+  __syncthreads();                     // no DMA in flight, every wave past its last LDS read
+
+  // Accumulator a = 2 i + j belongs to K-group a * KG / 4. The other groups
+  // leave their partial in LDS (lane-major, 4 KiB per block); the owner adds
+  // them in group order.
+  auto owner = [](int a) { return a * KG / 4; };
+  if constexpr (KG > 1) {
+    float* red = reinterpret_cast<float*>(lds);
+    auto slot = [&](int a, int k) {      // k != owner(a)
+      const int kk = k < owner(a) ? k : k - 1;
+      return red + (((size_t)pos * 4 + a) * (KG - 1) + kk) * 1024;
+    };
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+      if (owner(a) != kg) {
+        float* dst = slot(a, kg);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) dst[e * 64 + lane] = acc[a >> 1][a & 1][e];
+      }
+    __syncthreads();
+#pragma unroll
+    for (int a = 0; a < 4; ++a)
+      if (owner(a) == kg) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          float sum = 0.0f;
+#pragma unroll
+          for (int k = 0; k < KG; ++k) sum += (k == kg) ? acc[a >> 1][a & 1][e] : slot(a, k)[e * 64 + lane];
+          acc[a >> 1][a & 1][e] = sum;
+        }
+      }
+  }
+
+  // Epilogue of the owned blocks. Block (i, j), group q: activation row
+  // m0 + 64 wm + 32 i + r32, output columns n0 + 64 wn + 32 j + 8 q + 4 g + (0..3).
+#pragma unroll
+  for (int a = 0; a < 4; ++a) {
+    if (owner(a) != kg) continue;
+    const int i = a >> 1, j = a & 1;
+    const int row = m0 + wm * 64 + i * 32 + r32;
+    if (row >= p.M) continue;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int col = n0 + wn * 64 + j * 32 + 8 * q + 4 * g;
+      const f32x16& c = acc[i][j];
+      const float4 bv = *reinterpret_cast<const float4*>(p.bias + col);
+      float v[4] = {c[4 * q] + bv.x, c[4 * q + 1] + bv.y, c[4 * q + 2] + bv.z, c[4 * q + 3] + bv.w};
+      if constexpr (EPI == EPI_RESID) {
+        float4 gv = make_float4(1.0f, 1.0f, 1.0f, 1.0f);
+        if (p.gate) gv = *reinterpret_cast<const float4*>(p.gate + col);
+        float4* r = reinterpret_cast<float4*>(p.resid + (size_t)row * p.ldr + col);
+        float4 h = *r;
+        h.x += gv.x * v[0];
+        h.y += gv.y * v[1];
+        h.z += gv.z * v[2];
+        h.w += gv.w * v[3];
+        *r = h;
+      } else {
+        if constexpr (EPI == EPI_GELU) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = gelu_tanh(v[e]);
+        }
+        store4<bf16>(reinterpret_cast<bf16*>(p.out) + (size_t)row * p.ldo + col, v);
+      }
+    }
+  }
+}
+
+template <int BM, int BN, int NW, int EPI, int SITE, int KTB = 128, int STAGES = 4, int DIST = 3>
+hipError_t launch_cfg2(const GemmArgs& a, hipStream_t s) {
+  if (a.xq < 1 || (a.N / BN) % a.xq) return hipErrorInvalidValue;
+  dim3 grid((a.N / BN) * ((a.M + BM - 1) / BM));
+  launch((k_gemm2<BM, BN, NW, EPI, SITE, KTB, STAGES, DIST>), grid, dim3(64 * NW), 0, s, a);
+  return hipGetLastError();
 }
 
 template <typename T, int BM, int BN, int WGM, int WGN, int STAGES, int EPI, int SITE, int PF = 1>
@@ -314,50 +470,20 @@ hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// 64 x 64 tiles over `splits` K slices into f32 partials, then the reduction.
-template <typename T, int EPI, int SITE>
-hipError_t launch_splitk(const GemmArgs& a, int splits, float* ws, hipStream_t s) {
-  if (a.xq < 1 || (a.N / 64) % a.xq) return hipErrorInvalidValue;
-  GemmArgs pa = a;
-  pa.resid = ws;
-  dim3 grid((a.N / 64) * ((a.M + 63) / 64), 1, splits);
-  launch((k_gemm<T, 64, 64, 2, 2, 2, EPI_PARTIAL, SITE, 2>), grid, dim3(256), 0, s, pa);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  const int64_t total4 = (int64_t)a.M * a.N / 4;
-  launch((k_splitk_reduce<T, EPI, SITE>), dim3((unsigned)((total4 + 255) / 256)), dim3(256), 0, s, a, ws,
-                     splits);
-  return hipGetLastError();
-}
-
-// Tile choice for bf16 (fitted to measurements on MI355X at M = 820 ... 4096,
-// N = 1024 ... 4096, K = 1024 / 4096): estimated time = rounds of 256
-// workgroups x per-tile work / relative per-tile efficiency, with
-// 128 x 128 (8 waves) = 1, 64 x 128 = 0.72, 64 x 64 = 0.77. Long-K shapes that
-// fit in one round of 64 x 64 tiles are split in two along K when a workspace
-// is available (measured: two slices beat one and four at M = 820 ... 1310).
-struct TileChoice {
-  int cfg;       // 0: 128x128, 1: 64x128, 2: 64x64
-  int splits;
-};
-
-inline TileChoice choose_tiles(int M, int N, int K, int es, size_t ws_bytes) {
+// Tile choice for bf16 with K < 4096 (fitted to measurements on MI355X at
+// M = 820 ... 4096, N = 1024 ... 4096, K = 1024): estimated time = rounds of
+// 256 workgroups x per-tile work / relative per-tile efficiency, with
+// 128 x 128 (8 waves) = 1, 64 x 128 = 0.72, 64 x 64 = 0.77.
+inline int choose_tiles(int M, int N) {
   auto rounds = [&](int bm, int bn) { return (((long)(M + bm - 1) / bm) * (N / bn) + 255) / 256; };
   const double c128 = rounds(128, 128) * 16384.0;
   const double c64x128 = rounds(64, 128) * 8192.0 / 0.72;
   const double c64 = rounds(64, 64) * 4096.0 / 0.77;
-  TileChoice t{0, 1};
+  int cfg = 0;
   double best = c128;
-  if (c64x128 < best) { best = c64x128; t.cfg = 1; }
-  if (c64 < best) { best = c64; t.cfg = 2; }
-  const long t64 = ((long)(M + 63) / 64) * (N / 64);
-  const int kt = K * es / kBKB;
-  if (t.cfg == 2 && t64 <= 256 && kt >= 32) {
-    int splits = 1;
-    while (splits < 2 && t64 * splits * 2 <= 1024 && kt % (2 * splits) == 0) splits *= 2;
-    if ((size_t)splits * M * N * sizeof(float) <= ws_bytes) t.splits = splits;
-  }
-  return t;
+  if (c64x128 < best) { best = c64x128; cfg = 1; }
+  if (c64 < best) cfg = 2;
+  return cfg;
 }
 
 // Column groups of the XCD tile partition (see k_gemm): over the 8 XCDs, A is
@@ -386,15 +512,28 @@ inline int choose_xq(int M, int N, int K, int es, int BN) {
   return best;
 }
 
+// bf16: long K (>= 4096, the MLP's second projection) that fits one round of
+// 64 x 64 or 64 x 128 workgroups goes to k_gemm2 with four K-groups per
+// position (measured on MI355X at N = 1024, K = 4096: M = 820, 17.5 us against
+// 20.6 us for the best staged tile; M = 1310 ... 1915, 24.4 against 29.3 us);
+// everything else to the register-staged kernel.
 template <typename T, int EPI, int SITE>
-hipError_t launch_t(const GemmArgs& a0, float* ws, size_t ws_bytes, hipStream_t s) {
+hipError_t launch_t(const GemmArgs& a0, hipStream_t s) {
   GemmArgs a = a0;
   if constexpr (sizeof(T) == 2) {
-    const TileChoice t = choose_tiles(a.M, a.N, a.K, sizeof(T), ws ? ws_bytes : 0);
-    a.xq = choose_xq(a.M, a.N, a.K, sizeof(T), t.splits > 1 || t.cfg == 2 ? 64 : 128);
-    if (t.splits > 1) return launch_splitk<T, EPI, SITE>(a, t.splits, ws, s);
-    if (t.cfg == 0) return launch_cfg<T, 128, 128, 2, 4, 2, EPI, SITE, 2>(a, s);
-    if (t.cfg == 1) return launch_cfg<T, 64, 128, 2, 2, 2, EPI, SITE, 2>(a, s);
+    const long rows64 = (a.M + 63) / 64;
+    if (a.K >= 4096 && rows64 * (a.N / 64) <= 256) {
+      a.xq = choose_xq(a.M, a.N, a.K, 2, 64);
+      return launch_cfg2<64, 64, 4, EPI, SITE>(a, s);
+    }
+    if (a.K >= 4096 && rows64 * (a.N / 128) <= 256) {
+      a.xq = choose_xq(a.M, a.N, a.K, 2, 128);
+      return launch_cfg2<64, 128, 8, EPI, SITE>(a, s);
+    }
+    const int cfg = choose_tiles(a.M, a.N);
+    a.xq = choose_xq(a.M, a.N, a.K, 2, cfg == 2 ? 64 : 128);
+    if (cfg == 0) return launch_cfg<T, 128, 128, 2, 4, 2, EPI, SITE, 2>(a, s);
+    if (cfg == 1) return launch_cfg<T, 64, 128, 2, 2, 2, EPI, SITE, 2>(a, s);
     return launch_cfg<T, 64, 64, 2, 2, 2, EPI, SITE, 2>(a, s);
   } else {
     a.xq = choose_xq(a.M, a.N, a.K, sizeof(T), 128);
@@ -403,21 +542,21 @@ hipError_t launch_t(const GemmArgs& a0, float* ws, size_t ws_bytes, hipStream_t 
 }
 
 template <typename T>
-hipError_t launch_site(int site, int epi, const GemmArgs& a, float* ws, size_t wsb, hipStream_t s) {
+hipError_t launch_site(int site, int epi, const GemmArgs& a, hipStream_t s) {
   switch (site) {
-    case SITE_QKV: return launch_t<T, EPI_STORE, SITE_QKV>(a, ws, wsb, s);
-    case SITE_Q: return launch_t<T, EPI_STORE, SITE_Q>(a, ws, wsb, s);
-    case SITE_COND: return launch_t<T, EPI_STORE, SITE_COND>(a, ws, wsb, s);
-    case SITE_O: return launch_t<T, EPI_RESID, SITE_O>(a, ws, wsb, s);
-    case SITE_CO: return launch_t<T, EPI_RESID, SITE_CO>(a, ws, wsb, s);
-    case SITE_FC2: return launch_t<T, EPI_RESID, SITE_FC2>(a, ws, wsb, s);
-    case SITE_FC1: return launch_t<T, EPI_GELU, SITE_FC1>(a, ws, wsb, s);
+    case SITE_QKV: return launch_t<T, EPI_STORE, SITE_QKV>(a, s);
+    case SITE_Q: return launch_t<T, EPI_STORE, SITE_Q>(a, s);
+    case SITE_COND: return launch_t<T, EPI_STORE, SITE_COND>(a, s);
+    case SITE_O: return launch_t<T, EPI_RESID, SITE_O>(a, s);
+    case SITE_CO: return launch_t<T, EPI_RESID, SITE_CO>(a, s);
+    case SITE_FC2: return launch_t<T, EPI_RESID, SITE_FC2>(a, s);
+    case SITE_FC1: return launch_t<T, EPI_GELU, SITE_FC1>(a, s);
     default: break;
   }
   switch (epi) {
-    case EPI_STORE: return launch_t<T, EPI_STORE, SITE_OP>(a, ws, wsb, s);
-    case EPI_GELU: return launch_t<T, EPI_GELU, SITE_OP>(a, ws, wsb, s);
-    case EPI_RESID: return launch_t<T, EPI_RESID, SITE_OP>(a, ws, wsb, s);
+    case EPI_STORE: return launch_t<T, EPI_STORE, SITE_OP>(a, s);
+    case EPI_GELU: return launch_t<T, EPI_GELU, SITE_OP>(a, s);
+    case EPI_RESID: return launch_t<T, EPI_RESID, SITE_OP>(a, s);
   }
   return hipErrorInvalidValue;
 }
@@ -426,11 +565,10 @@ hipError_t launch_site(int site, int epi, const GemmArgs& a, float* ws, size_t w
 
 hipError_t launch_gemm(int site, int dt, int epi, int M, int N, int K, const void* A, int lda, const void* W,
                        int ldw, const float* bias, const float* gate, void* out, int ldo, float* resid, int ldr,
-                       float* ws, size_t ws_bytes, hipStream_t s) {
+                       hipStream_t s) {
   if (M == 0) return hipSuccess;
   GemmArgs a{M, N, K, (const char*)A, lda, (const char*)W, ldw, bias, gate, out, ldo, resid, ldr, 1};
-  return dt == DT_BF16 ? launch_site<bf16>(site, epi, a, ws, ws_bytes, s)
-                       : launch_site<float>(site, epi, a, ws, ws_bytes, s);
+  return dt == DT_BF16 ? launch_site<bf16>(site, epi, a, s) : launch_site<float>(site, epi, a, s);
 }
 
 }  // namespace f3c

@@ -17,7 +17,7 @@ struct Segs {
 };
 
 enum Dtype { DT_F32 = 0, DT_BF16 = 1 };
-enum Epilogue { EPI_STORE = 0, EPI_GELU = 1, EPI_RESID = 2, EPI_PARTIAL = 3 };
+enum Epilogue { EPI_STORE = 0, EPI_GELU = 1, EPI_RESID = 2 };
 
 // Call sites of the dense kernels. Each site is its own template instance, so a
 // kernel trace attributes time to the projection / attention it belongs to.
@@ -70,11 +70,11 @@ hipError_t launch_convert(int dt, const float* src, void* dst, int64_t n, hipStr
 // C = A W^T + bias with an epilogue. A: [M][lda], W: [N][ldw] (model dtype),
 // bias f32 [N]. EPI_STORE / EPI_GELU write out[M][ldo] in the model dtype;
 // EPI_RESID does resid[m][n] += (gate ? gate[n] : 1) * value in f32.
-// Requires N % 128 == 0 and K % (128 / sizeof(element)) == 0. ws (f32, ws_bytes)
-// may be null; when present, small-M long-K shapes are split along K into it.
+// Requires N % 128 == 0 and K % (128 / sizeof(element)) == 0. Each output is
+// one workgroup's sum in a fixed order.
 hipError_t launch_gemm(int site, int dt, int epi, int M, int N, int K, const void* A, int lda, const void* W,
                        int ldw, const float* bias, const float* gate, void* out, int ldo, float* resid, int ldr,
-                       float* ws, size_t ws_bytes, hipStream_t s);
+                       hipStream_t s);
 
 // Varlen multi-head softmax attention. Queries of sample b are rows
 // [qs.off[b], qs.off[b+1]) of q; its keys/values are rows [ks.off[b], ks.off[b+1])

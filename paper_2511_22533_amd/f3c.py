@@ -76,7 +76,7 @@ _SIGS = {
     "f3c_profile_reset": (c_int, [c_p]),
     "f3c_op_select": (c_int, [c_int, c_int, c_p, c_p, c_f, P_i32, c_p, c_p, c_p, c_p]),
     "f3c_op_gemm": (c_int, [c_int, c_int, c_int, c_int, c_int, c_p, c_int, c_p, c_int, c_p, c_p, c_p, c_int, c_p,
-                            c_int, c_p, c_sz, c_p]),
+                            c_int, c_p]),
     "f3c_op_attention": (c_int, [c_int, c_int, c_int, c_int, P_i32, P_i32, c_p, c_int, c_p, c_int, c_p, c_int, c_p,
                                  c_int, c_p, c_sz, c_p]),
     "f3c_op_ln_mod": (c_int, [c_int, c_int, c_int, c_p, c_p, c_p, c_p, c_p]),
@@ -387,14 +387,12 @@ def op_select(v_cache, v_prev, omega: float, n_cache: Sequence[int], idx_active,
                               idx_active.data_ptr(), pos.data_ptr(), _ptr(score), _stream(stream)))
 
 
-def op_gemm(dtype: int, epilogue: int, A, W, bias, out=None, resid=None, gate=None, workspace=None, stream=None):
+def op_gemm(dtype: int, epilogue: int, A, W, bias, out=None, resid=None, gate=None, stream=None):
     M, K = A.shape
     N = W.shape[0]
-    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     check(lib().f3c_op_gemm(dtype, epilogue, M, N, K, A.data_ptr(), A.stride(0), W.data_ptr(), W.stride(0),
                             bias.data_ptr(), _ptr(gate), _ptr(out), out.stride(0) if out is not None else 0,
-                            _ptr(resid), resid.stride(0) if resid is not None else 0, _ptr(workspace), ws_bytes,
-                            _stream(stream)))
+                            _ptr(resid), resid.stride(0) if resid is not None else 0, _stream(stream)))
 
 
 def op_attention(dtype: int, heads: int, head_dim: int, q_off, k_off, q, k, v, o, workspace=None, stream=None):

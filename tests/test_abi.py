@@ -114,9 +114,9 @@ def test_op_entry_validation_is_host_side(L):
     assert L.f3c_op_select(1, 512, 1, 1, 1.5, q, 1, 1, None, None) == f3c.F3C_EINVAL
     assert L.f3c_op_select(1, 4, 1, 1, 0.7, f3c._i32([5]), 1, 1, None, None) == f3c.F3C_EINVAL
     assert L.f3c_op_select(1, 40000, 1, 1, 0.7, f3c._i32([5]), 1, 1, None, None) == f3c.F3C_EINVAL
-    assert L.f3c_op_gemm(1, 0, 16, 100, 64, 1, 64, 1, 64, 1, None, 1, 100, None, 0, None, 0, None) == f3c.F3C_EINVAL
-    assert L.f3c_op_gemm(1, 0, 16, 128, 40, 1, 40, 1, 40, 1, None, 1, 128, None, 0, None, 0, None) == f3c.F3C_EINVAL
-    assert L.f3c_op_gemm(1, 0, 16, 128, 64, 1, 64, 1, 64, 1, None, 1, 130, None, 0, None, 0, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_gemm(1, 0, 16, 100, 64, 1, 64, 1, 64, 1, None, 1, 100, None, 0, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_gemm(1, 0, 16, 128, 40, 1, 40, 1, 40, 1, None, 1, 128, None, 0, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_gemm(1, 0, 16, 128, 64, 1, 64, 1, 64, 1, None, 1, 130, None, 0, None) == f3c.F3C_EINVAL
     assert L.f3c_op_attention(1, 4, 48, 1, q, q, 1, 192, 1, 192, 1, 192, 1, 192, None, 0, None) == f3c.F3C_EINVAL
     assert L.f3c_op_attention(1, 4, 64, 1, f3c._i32([0, 3]), f3c._i32([0, 0]), 1, 256, 1, 256, 1, 256, 1, 256,
                               None, 0, None) == f3c.F3C_EINVAL
