@@ -222,8 +222,9 @@ def test_cross_attention_bf16(torch, q_lens):
 
 
 # With a workspace, launches with few query tiles split the key range and
-# merge the partial results in a fixed order. Splits chosen for these cases:
-# 2, 2, 2, 2, 4, 8, and none for the last two.
+# merge the partial results in a fixed order. Chosen for these cases (bf16,
+# 16 heads): two key groups in one workgroup, key groups, key groups, 2
+# splits, 4 splits, 8 splits, key groups, key groups.
 @pytest.mark.parametrize("q_lens,k_lens", [([1000], [1000]), ([820], [1374]), ([5, 300, 0, 77], [1374] * 4),
                                            ([300], [1374]), ([1, 40], [4096, 2000]), ([64], [8192]),
                                            ([1310], [1310]), ([820], [820])])
@@ -247,6 +248,14 @@ def test_attention_bf16_growing_scores(torch, q_lens, k_lens, ramp, ws):
     from paper_2511_22533_amd import f3c
     assert _attn_case(torch, f3c.F3C_BF16, 16, 64, q_lens, k_lens, seed=int(10 * ramp) + len(q_lens),
                       workspace=ws, key_ramp=ramp, sample_queries=128) < 2e-2
+
+
+# Two key groups with one or two key tiles: the second group's only tile lies
+# past the end (all keys masked) or is the ragged last one.
+@pytest.mark.parametrize("q_lens,k_lens", [([600], [50]), ([600], [64]), ([700], [100]), ([5, 600], [1, 65])])
+def test_attention_bf16_key_groups_short_keys(torch, q_lens, k_lens):
+    from paper_2511_22533_amd import f3c
+    assert _attn_case(torch, f3c.F3C_BF16, 16, 64, q_lens, k_lens, seed=sum(k_lens)) < 2e-2
 
 
 @pytest.mark.parametrize("hd,heads", [(32, 4), (64, 2)])
