@@ -176,6 +176,15 @@ int f3c_state_views(const f3c_state* s, float** v_cache, float** v_prev, int32_t
                     float** v_act, float** mod, float** score, int32_t* act_off_host);
 int f3c_state_record_scores(f3c_state* s, int32_t on);
 
+/* Debug: while h_trace_dev is set (device, 16-byte aligned, bytes long), every
+ * step also copies the transformer's residual stream h (float32 [rows][width],
+ * rows = the step's active rows, both passes on a guided step) after the
+ * embedding and after each block l into slices 0 and l + 1 of h_trace_dev
+ * ([L + 1][rows][width]); a step whose slices do not fit fails with
+ * F3C_ENOMEM before enqueuing anything. NULL turns it off. It serves the
+ * per-block parity of the transformer (the change each block makes to h). */
+int f3c_state_trace_blocks(f3c_state* s, float* h_trace_dev, size_t bytes);
+
 /* Checkpoint: the sampler state beyond x is the cache pair. export copies
  * v_cache then v_prev (2*B*N*8 floats) to host memory; import restores them.
  * Both synchronise `stream`. */

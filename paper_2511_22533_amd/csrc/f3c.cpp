@@ -94,6 +94,8 @@ struct f3c_state {
   float* ws = nullptr;          // attention key-split partials
   size_t ws_bytes = 0;
   bool guided = false;          // activations and condition K/V sized for two passes per sample
+  float* trace = nullptr;       // debug: residual stream after the embedding and after each block
+  size_t trace_bytes = 0;
   bool cond_set = false, uncond_set = false, record_scores = false;
   uint32_t prof_mask = 0;
   float omega = 0.7f;
@@ -261,6 +263,8 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
     auto proj_bytes = [&](double n, double k, bool resid) { return (r * k + n * k) * E + r * n * (resid ? 8.0 : E); };
     double cond_rows = 0;
     for (int g = 0; g < P * B; ++g) cond_rows += (tact.off[g + 1] > tact.off[g]) ? m->Nc : 0;
+    const size_t hslice = (size_t)rows * d;       // trace size checked by step_common
+    if (s->trace) HIP_TRY(hipMemcpyAsync(s->trace, s->h, hslice * 4, hipMemcpyDeviceToDevice, st));
     for (int l = 0; l < L; ++l) {
       const std::string p = "blk" + std::to_string(l) + ".";
       const float* md = s->mod + (size_t)l * 6 * d;
@@ -321,6 +325,8 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
         HIP_TRY(launch_gemm(SITE_FC2, dt, EPI_RESID, rows, d, dm, s->hid, dm, m->w(p + "fc2_w"), dm, m->b(p + "fc2_b"),
                             md + 5 * d, nullptr, 0, s->h, d, st));
       }
+      if (s->trace)
+        HIP_TRY(hipMemcpyAsync(s->trace + (l + 1) * hslice, s->h, hslice * 4, hipMemcpyDeviceToDevice, st));
     }
     {
       Scope sc(s, F3C_PROF_FINAL, st, 0, rows * (d * 4.0 + 32));
@@ -646,6 +652,12 @@ static int step_common(f3c_state* s, float* x, double t, double t_next, const in
     for (int b = 0; b < s->B; ++b)
       if (n_cache[b] < 0 || n_cache[b] > s->m->N)
         return fail(F3C_EINVAL, "n_cache[%d] = %d outside [0, %d]", b, n_cache[b], s->m->N);
+  if (s->trace) {
+    size_t rows = 0;
+    for (int b = 0; b < s->B; ++b) rows += s->m->N - (n_cache ? n_cache[b] : 0);
+    const size_t need = (size_t)(s->m->L + 1) * rows * (guide ? 2 : 1) * s->m->d * sizeof(float);
+    if (need > s->trace_bytes) return fail(F3C_ENOMEM, "trace buffer %zu < %zu bytes", s->trace_bytes, need);
+  }
   if (guide) {
     if (!s->guided) return fail(F3C_ESTATE, "state was not created with F3C_STATE_GUIDED");
     if (!s->uncond_set) return fail(F3C_ESTATE, "unconditional input not set (call f3c_set_uncond first)");
@@ -681,6 +693,14 @@ int f3c_state_views(const f3c_state* s, float** v_cache, float** v_prev, int32_t
   if (score) *score = s->score;
   if (act_off_host)
     for (int b = 0; b <= s->B; ++b) act_off_host[b] = s->last_act.off[b];
+  return F3C_OK;
+}
+
+int f3c_state_trace_blocks(f3c_state* s, float* h_trace_dev, size_t bytes) {
+  if (!s) return fail(F3C_EINVAL, "state is NULL");
+  if (h_trace_dev && ((uintptr_t)h_trace_dev & 15)) return fail(F3C_EINVAL, "trace buffer must be 16-byte aligned");
+  s->trace = h_trace_dev;
+  s->trace_bytes = h_trace_dev ? bytes : 0;
   return F3C_OK;
 }
 

@@ -61,6 +61,7 @@ _SIGS = {
     "f3c_set_uncond": (c_int, [c_p, c_p, c_p]),
     "f3c_guided_step": (c_int, [c_p, c_p, c_d, c_d, P_i32, c_d, c_p]),
     "f3c_guidance_active": (c_int, [c_d, c_d, c_d]),
+    "f3c_state_trace_blocks": (c_int, [c_p, c_p, c_sz]),
     "f3c_state_destroy": (None, [c_p]),
     "f3c_state_reset": (c_int, [c_p, c_p]),
     "f3c_state_set_omega": (c_int, [c_p, c_f]),
@@ -298,6 +299,10 @@ class State:
         check(lib().f3c_guided_step(self.h, x.data_ptr(), t, t_next, None if n_cache is None else _i32(n_cache), w,
                                     _stream(stream)))
         self.last_guided = True
+
+    def trace_blocks(self, buf=None):
+        """Debug: copy the residual stream after the embedding and each block into buf (f32 device tensor)."""
+        check(lib().f3c_state_trace_blocks(self.h, _ptr(buf), buf.numel() * 4 if buf is not None else 0))
 
     def record_scores(self, on: bool):
         check(lib().f3c_state_record_scores(self.h, int(on)))

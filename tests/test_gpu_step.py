@@ -406,3 +406,50 @@ def test_guided_step_preconditions(torch):
     torch.cuda.synchronize()
     assert torch.equal(x, x2)
 
+
+
+@pytest.mark.parametrize("case", ["tiny_f32", "trellis16_bf16", "trellis16_bf16_guided"])
+def test_per_block_residual_changes(torch, case):
+    """The change each block makes to the residual stream (its gated
+    self-attention, cross-attention and MLP outputs) against the oracle's, on
+    the GPU's own active set, plus the embedding. With random-init gates
+    (about 0.03) a wrong sublayer moves the final velocity too little for the
+    velocity tolerance; the per-block change exposes it."""
+    from paper_2511_22533_amd import f3c
+    guided = case.endswith("guided")
+    cfg = synth.TINY if case == "tiny_f32" else depth_variant(synth.TRELLIS16, 2)
+    B = 2 if case == "tiny_f32" else 1
+    pair = Pair(cfg, B, uncond=synth.make_cond(cfg, B, seed_base=2500) if guided else None)
+    rng = np.random.default_rng(13)
+    vc = (0.5 * rng.standard_normal((B, cfg.tokens, 8))).astype(F32)
+    vp = (vc + 0.05 * rng.standard_normal(vc.shape)).astype(F32)
+    pair.state.import_(np.concatenate([vc.ravel(), vp.ravel()]))
+    q = [100, 300] if case == "tiny_f32" else [2048]
+    rows = sum(cfg.tokens - c for c in q) * (2 if guided else 1)
+    L, d = cfg.depth, cfg.width
+    buf = torch.zeros(((L + 1) * rows * d,), dtype=torch.float32, device="cuda")
+    pair.state.trace_blocks(buf)
+    x = to_dev(pair.x_T)
+    say("per-block parity", case, q)
+    r = _gpu_step(torch, pair, x, 0.7, 0.65, q, 2.0 if guided else None)
+    pair.state.trace_blocks(None)
+    tr_gpu = buf.cpu().numpy().reshape(L + 1, rows, d).astype(np.float64)
+    tol_e, tol_dh = (1e-5, 1e-4) if cfg.dtype == "f32" else (1e-5, 1.5e-2)
+    n_act = rows // (2 if guided else 1)
+    worst = 0.0
+    for p_idx, cond in enumerate([pair.cond] + ([pair.uncond] if guided else [])):
+        for b in range(B):
+            lo, hi = r["off"][b] + p_idx * n_act, r["off"][b + 1] + p_idx * n_act
+            active = r["idx"][r["off"][b]:r["off"][b + 1]] if any(q) else np.arange(cfg.tokens)
+            tr = {}
+            pair.oracle.forward(r["x0"][b][active], active, 0.7, cond[b], trace=tr)
+            assert max_rel(tr_gpu[0][lo:hi], tr["embed"]) < tol_e
+            prev_gpu, prev_ref = tr_gpu[0][lo:hi], tr["embed"]
+            for l in range(L):
+                dh_gpu = tr_gpu[l + 1][lo:hi] - prev_gpu
+                dh_ref = tr[l]["h"] - prev_ref
+                err = max_rel(dh_gpu, dh_ref)
+                worst = max(worst, err)
+                assert err < tol_dh, f"pass {p_idx} sample {b} block {l}: {err}"
+                prev_gpu, prev_ref = tr_gpu[l + 1][lo:hi], tr[l]["h"]
+    say("per-block worst max-rel", worst)
