@@ -50,6 +50,10 @@ def parse():
     ap.add_argument("--copy-ref-mb", type=int, default=0,
                     help="first run one plain device-to-device copy of this many MiB (a known-size reference "
                          "for hardware byte counters)")
+    ap.add_argument("--log-steps", action="store_true",
+                    help="after the timed region, run one more trajectory and print one JSON line per step to "
+                         "stderr (k, t, quotas, active tokens, model FLOPs, wall time, per-class kernel times); "
+                         "every class is profiled there, so its wall times include the event stamps")
     ap.add_argument("--hbm-sweep", action="store_true",
                     help="instead of the sampler: time the memory-bound kernels in isolation over a size sweep "
                          "and report algorithmic bytes / kernel time against HBM peak")
@@ -377,6 +381,27 @@ def main():
     q_min = quotas[k_min].tolist()
     cached_ms = _event_time_ms(torch, lambda: state.cached_step(x, float(times[k_min]), float(times[k_min + 1]),
                                                                 q_min), 20) if any(q_min) else None
+
+    if args.log_steps:
+        # One trajectory, untimed for `value`: per-step wall time between events
+        # on the launch stream, and the library's per-class kernel times.
+        state.profile(True)
+        for k in range(T):
+            state.profile_reset()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            n_act = run_step(k)
+            e1.record()
+            e1.synchronize()
+            cls = state.profile_read()
+            rec = {"k": k + 1, "t": float(times[k]), "t_next": float(times[k + 1]),
+                   "n_cache": quotas[k].tolist(), "n_active": int(n_act), "guided": bool(guided[k]),
+                   "model_flops": (2 if guided[k] else 1) * sum(f3c.forward_flops(cfg, cfg.tokens - int(c), 1)
+                                                                 for c in quotas[k]),
+                   "wall_ms": round(e0.elapsed_time(e1), 4),
+                   "class_ms": {c: round(v["ms"], 4) for c, v in cls.items() if v["launches"]}}
+            print(json.dumps(rec), file=sys.stderr, flush=True)
+        state.profile(False)
 
     peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
     achieved = prof["flops"] / (prof["ms"] * 1e-3) / 1e12 if prof["ms"] > 0 else 0.0
