@@ -717,34 +717,47 @@ inline size_t split_bytes(int splits, int rows, int heads, int hd) {
 }
 
 // 8 waves (256 queries) per workgroup when that still gives at least 160
-// workgroups, else 128 queries per workgroup: eight waves in two key groups
-// (bf16, 64-wide heads) or four waves. Eight waves share each staged K/V
-// tile, which halves the staging work per query; measured on MI355X from 300
-// to 4096 queries, 256-query workgroups lead from about 2300 queries up.
-// With few query tiles the key range is split over workgroups, only while all
-// of them still fit in one round on 256 CUs and every split keeps at least 8
-// key tiles: below that the partial-result traffic and the merge launch cost
-// more than the parallelism.
+// workgroups; measured on MI355X from 300 to 4096 queries, 256-query
+// workgroups lead from about 2300 queries up (eight waves share each staged
+// K/V tile, which halves the staging work per query). Below that the time is
+// the serial chain of key tiles that one wave walks. Two ways shorten it:
+//  * key groups (bf16, 64-wide heads): the waves of a workgroup split into two
+//    key groups merged through LDS; 64-query workgroups of four waves while
+//    they fit one round on the 256 CUs (128 KiB of LDS: one per CU), else
+//    128-query workgroups of eight waves. Chain: half the key tiles.
+//  * key-range splits over workgroups of four waves, merged by a second
+//    kernel, while all of them fit one round and every split keeps at least
+//    8 key tiles. Chain: 1/splits of the key tiles, plus the merge.
+// Measured on MI355X, 16 heads: both cost about 0.85 us per tile of chain,
+// and splits about 4.5 us more in fixed cost, so key groups are taken unless
+// splits shorten the chain by more than kSplitGainTiles. Examples: self 820
+// queries 10.7 us (key groups) against 13.6 (eight waves, key groups); cross
+// 820 x 1374 keys 14.6 against 19.2 (two splits); 64 x 4096 keys 29.7 against
+// 16.4 (eight splits). Other types and head sizes: four waves, with splits.
+constexpr long kSplitGainTiles = 5;
+
 template <int SITE>
 hipError_t launch_site(int dt, int hd, const AttnArgs& a, int heads, float* ws, size_t ws_bytes, hipStream_t s) {
-  long t128 = 0, t256 = 0, kt_min = 1L << 30;
+  long t64 = 0, t128 = 0, t256 = 0, kt_min = 1L << 30, kt_max = 0;
   for (int b = 0; b < a.qs.B; ++b) {
     const int nq = a.qs.off[b + 1] - a.qs.off[b];
     if (nq == 0) continue;
+    t64 += (nq + 63) / 64;
     t128 += (nq + 127) / 128;
     t256 += (nq + 255) / 256;
-    kt_min = std::min<long>(kt_min, (a.ks.off[b + 1] - a.ks.off[b] + kBKV - 1) / kBKV);
+    const long kt = (a.ks.off[b + 1] - a.ks.off[b] + kBKV - 1) / kBKV;
+    kt_min = std::min(kt_min, kt);
+    kt_max = std::max(kt_max, kt);
   }
   if (t256 * heads >= 160) return launch_a<8, SITE>(dt, hd, a, heads, 1, s);
-  // Between that and a few query tiles, 128-query workgroups of eight waves in
-  // two key groups (measured on MI355X, 16 heads: self-attention at 1128 to
-  // 1915 queries 8-12% faster than four waves, cross-attention at 820 to 1915
-  // queries 7-10% faster than four waves or two key-range splits).
-  if (dt == DT_BF16 && hd == 64 && t128 * heads > 64) return launch_a<8, SITE, 2>(dt, hd, a, heads, 1, s);
   int splits = 1;
   while (splits < 8 && t128 * heads * splits * 2 <= 256 && kt_min >= 16 * splits) splits *= 2;
   const int rows = a.qs.off[a.qs.B] - a.qs.off[0];
   while (splits > 1 && (!ws || split_bytes(splits, rows, heads, hd) > ws_bytes)) splits /= 2;
+  if (dt == DT_BF16 && hd == 64 && (kt_max + 1) / 2 - (kt_max + splits - 1) / splits <= kSplitGainTiles) {
+    if (t64 * heads <= 256) return launch_a<4, SITE, 2>(dt, hd, a, heads, 1, s);
+    return launch_a<8, SITE, 2>(dt, hd, a, heads, 1, s);
+  }
   AttnArgs b = a;
   if (splits > 1) {
     b.part_o = ws;

@@ -221,10 +221,12 @@ def test_cross_attention_bf16(torch, q_lens):
     assert _attn_case(torch, f3c.F3C_BF16, 16, 64, q_lens, [1374] * len(q_lens), seed=len(q_lens)) < 2e-2
 
 
-# With a workspace, launches with few query tiles split the key range and
-# merge the partial results in a fixed order. Chosen for these cases (bf16,
-# 16 heads): two key groups in one workgroup, key groups, key groups, 2
-# splits, 4 splits, 8 splits, key groups, key groups.
+# With a workspace, launches with few query tiles may split the key range
+# over workgroups and merge the partial results in a fixed order; they do
+# when that shortens each wave's chain of key tiles by more than five tiles
+# against two key groups in one workgroup. Chosen for these cases (bf16, 16
+# heads): key groups of four waves for the first four, 4 splits, 8 splits,
+# key groups of eight waves, key groups of four waves.
 @pytest.mark.parametrize("q_lens,k_lens", [([1000], [1000]), ([820], [1374]), ([5, 300, 0, 77], [1374] * 4),
                                            ([300], [1374]), ([1, 40], [4096, 2000]), ([64], [8192]),
                                            ([1310], [1310]), ([820], [820])])
@@ -240,9 +242,10 @@ def test_attention_bf16_split_keys(torch, q_lens, k_lens):
 # Scores that grow from tile to tile: the running reference max of the
 # matrix-core path is too small for later tiles, so its fix-up branch
 # (rescale what was accumulated, redo the tile) runs, for some queries of a
-# wave and not others; in the four-wave, eight-wave and key-split launches.
+# wave and not others; in the four-wave key-group, eight-wave and key-split
+# (300 x 4096 keys: 4 splits) launches.
 @pytest.mark.parametrize("q_lens,k_lens,ramp,ws", [([300], [300], 2.0, False), ([1000], [1000], 0.5, False),
-                                                   ([820], [1374], 1.0, False), ([300], [1374], 2.0, True),
+                                                   ([820], [1374], 1.0, False), ([300], [4096], 0.5, True),
                                                    ([37, 3000], [37, 3000], 0.3, False), ([640], [640], 0.12, False)])
 def test_attention_bf16_growing_scores(torch, q_lens, k_lens, ramp, ws):
     from paper_2511_22533_amd import f3c
@@ -251,8 +254,10 @@ def test_attention_bf16_growing_scores(torch, q_lens, k_lens, ramp, ws):
 
 
 # Two key groups with one or two key tiles: the second group's only tile lies
-# past the end (all keys masked) or is the ragged last one.
-@pytest.mark.parametrize("q_lens,k_lens", [([600], [50]), ([600], [64]), ([700], [100]), ([5, 600], [1, 65])])
+# past the end (all keys masked) or is the ragged last one; four-wave
+# workgroups up to 1024 queries, eight-wave ones at 1100.
+@pytest.mark.parametrize("q_lens,k_lens", [([600], [50]), ([600], [64]), ([700], [100]), ([5, 600], [1, 65]),
+                                           ([1100], [50]), ([1100], [100])])
 def test_attention_bf16_key_groups_short_keys(torch, q_lens, k_lens):
     from paper_2511_22533_amd import f3c
     assert _attn_case(torch, f3c.F3C_BF16, 16, 64, q_lens, k_lens, seed=sum(k_lens)) < 2e-2

@@ -255,12 +255,12 @@ def test_profiler_times_kernels_and_leaves_results_unchanged(torch):
     """With every class profiled, launches go through the event-stamping
     extended launch: the step's results stay bit-identical, every class that
     launched has a positive time, and the class times fit inside the step's
-    wall time. The condition is long enough (1100 tokens) and the active set
-    small enough (112 tokens) that cross-attention splits its key range, so a
-    class of two kernels is timed too."""
+    wall time. The condition is long enough (4096 tokens, 64 key tiles) and the
+    active set small enough (112 tokens) that cross-attention splits its key
+    range over workgroups, so a class of two kernels is timed too."""
     from paper_2511_22533_amd import f3c
     from paper_2511_22533_amd.f3c import PROF_CLASSES
-    cfg = synth.ModelConfig(grid=8, width=256, depth=2, heads=4, cond_tokens=1100, cond_width=64, dtype="bf16")
+    cfg = synth.ModelConfig(grid=8, width=256, depth=2, heads=4, cond_tokens=4096, cond_width=64, dtype="bf16")
     model = f3c.Model(cfg).load(synth.make_weights(cfg, seed=0))
     state = f3c.State(model, 1)
     cond = to_dev(synth.make_cond(cfg, 1))
