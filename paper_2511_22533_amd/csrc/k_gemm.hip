@@ -19,6 +19,8 @@
 // vectors. A lane reads 16 contiguous bytes of one row at K-group offset l/32
 // for both operands; any common assignment of K elements to the instruction's
 // K slots yields the same dot products.
+#include <cmath>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -470,19 +472,28 @@ hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Tile choice for bf16 with K < 4096 (fitted to measurements on MI355X at
-// M = 820 ... 4096, N = 1024 ... 4096, K = 1024): estimated time = rounds of
-// 256 workgroups x per-tile work / relative per-tile efficiency, with
-// 128 x 128 (8 waves) = 1, 64 x 128 = 0.72, 64 x 64 = 0.77.
-inline int choose_tiles(int M, int N) {
-  auto rounds = [&](int bm, int bn) { return (((long)(M + bm - 1) / bm) * (N / bn) + 255) / 256; };
-  const double c128 = rounds(128, 128) * 16384.0;
-  const double c64x128 = rounds(64, 128) * 8192.0 / 0.72;
-  const double c64 = rounds(64, 64) * 4096.0 / 0.77;
+// Tile choice for the register-staged bf16 kernel: the smallest estimated
+// time over 128 x 128 (8 waves), 64 x 128 and 64 x 64 (4 waves) tiles. Model
+// per tile shape: a fixed cost plus, per 1024 of K, a cost per round of 256
+// workgroups (a partial round costs a whole one) and a smaller cost per
+// workgroup (L2 and HBM contention); least-squares fit to 52 measurements on
+// MI355X with random bf16 operands at M = 820 ... 4055, N = 1024 / 3072 /
+// 4096, K = 1024 / 4096 (rms 1.1 / 1.8 / 1.1 us). Over those shapes it picks
+// within 0.2% of the best tile in total time (the earlier rounds-only model:
+// 1.4%, up to 11% on single shapes).
+inline int choose_tiles(int M, int N, int K) {
+  struct Cost { int bm, bn; double fixed, per_round, per_load; };
+  constexpr Cost kCost[3] = {{128, 128, 6.37, 6.73, 2.86}, {64, 128, 6.16, 4.85, 1.10}, {64, 64, 5.35, 2.51, 0.85}};
   int cfg = 0;
-  double best = c128;
-  if (c64x128 < best) { best = c64x128; cfg = 1; }
-  if (c64 < best) cfg = 2;
+  double best = 0.0;
+  for (int c = 0; c < 3; ++c) {
+    const double load = (double)((M + kCost[c].bm - 1) / kCost[c].bm) * (N / kCost[c].bn) / 256.0;
+    const double t = kCost[c].fixed + K / 1024.0 * (kCost[c].per_round * std::ceil(load) + kCost[c].per_load * load);
+    if (c == 0 || t < best) {
+      best = t;
+      cfg = c;
+    }
+  }
   return cfg;
 }
 
@@ -530,7 +541,7 @@ hipError_t launch_t(const GemmArgs& a0, hipStream_t s) {
       a.xq = choose_xq(a.M, a.N, a.K, 2, 128);
       return launch_cfg2<64, 128, 8, EPI, SITE>(a, s);
     }
-    const int cfg = choose_tiles(a.M, a.N);
+    const int cfg = choose_tiles(a.M, a.N, a.K);
     a.xq = choose_xq(a.M, a.N, a.K, 2, cfg == 2 ? 64 : 128);
     if (cfg == 0) return launch_cfg<T, 128, 128, 2, 4, 2, EPI, SITE, 2>(a, s);
     if (cfg == 1) return launch_cfg<T, 64, 128, 2, 2, 2, EPI, SITE, 2>(a, s);

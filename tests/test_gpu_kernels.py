@@ -129,8 +129,10 @@ def _gemm_case(torch, dt, epi, M, N, K, seed):
     return got, want
 
 
+# Tile shapes picked: 64 x 64 for the first four, 128 x 128 for 4096 x 1024 x
+# 4096 and 2057 x 4096, 64 x 128 for 1310 x 3072.
 @pytest.mark.parametrize("M,N,K", [(1, 128, 64), (37, 384, 128), (128, 1024, 1024), (820, 3072, 1024),
-                                   (4096, 1024, 4096), (2057, 4096, 1024)])
+                                   (4096, 1024, 4096), (2057, 4096, 1024), (1310, 3072, 1024)])
 @pytest.mark.parametrize("epi", [0, 1, 2])
 def test_gemm_bf16(torch, M, N, K, epi):
     from paper_2511_22533_amd import f3c
