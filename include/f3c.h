@@ -244,10 +244,12 @@ int f3c_op_gemm(int32_t dtype, int32_t epilogue, int32_t M, int32_t N, int32_t K
  * head h uses columns h*head_dim..; o (T) gets one row per query.
  * head_dim in {32, 64}; offsets are host arrays of B+1 non-decreasing ints.
  * workspace (device, 16-byte aligned, may be NULL) lets launches with few
- * query tiles split the key range: each split's unnormalised output, max and
- * sum go to the workspace (splits * rows * heads * (head_dim + 2) floats) and
- * are merged in split order, so results do not depend on scheduling. The
- * split count shrinks to what the workspace holds. */
+ * query tiles and long key ranges split the key range over workgroups (when
+ * that shortens each wave's chain of key tiles by enough to repay the merge):
+ * each split's unnormalised output, max and sum go to the workspace (splits *
+ * rows * heads * (head_dim + 2) floats) and are merged in split order, so
+ * results do not depend on scheduling. The split count shrinks to what the
+ * workspace holds; without a workspace nothing is split. */
 int f3c_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int32_t batch, const int32_t* q_off_host,
                      const int32_t* k_off_host, const void* q, int32_t ldq, const void* k, int32_t ldk,
                      const void* v, int32_t ldv, void* o, int32_t ldo, float* workspace, size_t workspace_bytes,
