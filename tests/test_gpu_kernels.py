@@ -204,8 +204,12 @@ def _attn_case(torch, dt, heads, hd, q_lens, k_lens, seed, sample_queries=None, 
     return worst
 
 
+# 1024 and 1025 queries sit on either side of the switch from four-wave to
+# eight-wave key-group workgroups (16 x 16 = 256 workgroups of 64 queries is
+# the last grid that fits one round).
 @pytest.mark.parametrize("q_lens,k_lens", [([64], [64]), ([1], [1]), ([200], [200]), ([0, 37, 300], [0, 37, 300]),
-                                           ([820], [820]), ([615, 1536, 2458, 1003], [615, 1536, 2458, 1003])])
+                                           ([820], [820]), ([615, 1536, 2458, 1003], [615, 1536, 2458, 1003]),
+                                           ([1024], [1024]), ([1025], [1025])])
 def test_self_attention_bf16(torch, q_lens, k_lens):
     from paper_2511_22533_amd import f3c
     assert _attn_case(torch, f3c.F3C_BF16, 16, 64, q_lens, k_lens, seed=sum(q_lens)) < 2e-2
