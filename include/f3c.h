@@ -20,6 +20,11 @@
  * alive until the model / state is destroyed. Host-side objects (f3c_model,
  * f3c_state) are owned by the library and released by the destroy calls.
  *
+ * Concurrency: a model holds only its weights (read-only once loaded); every
+ * buffer a step writes belongs to its state. Several states of one model may
+ * therefore step concurrently on different streams. Calls on one state must
+ * be ordered, normally by issuing them on one stream.
+ *
  * Layouts: latent grids and velocities are float32 [B][N][8], token-major,
  * with token n = (z*G + y)*G + x for an G x G x G grid (the flatten order of
  * the D x H x W latent, Sec. 4.2). Condition tokens are float32 [B][Nc][dc].

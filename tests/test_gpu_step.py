@@ -181,6 +181,42 @@ def test_checkpoint_resume_bit_identical(torch):
     assert torch.equal(first, x)
 
 
+def test_two_states_on_two_streams_match_sequential(torch):
+    """Every per-step buffer lives in the state and the model holds only
+    weights, so two states of one model stepping on two streams at once
+    (launches interleaved, nothing orders one stream against the other) give
+    bit for bit what they give stepping on one stream."""
+    from paper_2511_22533_amd import f3c
+    cfg = depth_variant(synth.TRELLIS16, 2)
+    model = f3c.Model(cfg).load(synth.make_weights(cfg, seed=0))
+    states = [f3c.State(model, 1) for _ in range(2)]
+    conds = [to_dev(synth.make_cond(cfg, 1, seed_base=2000 + 10 * i)) for i in range(2)]
+    x_T = [synth.make_noise(cfg, 1, seed_base=1000 + 10 * i) for i in range(2)]
+    times = schedule.time_grid(6, 3.0)
+    quotas = [[0], [0], [1024], [2048], [3000], [3276]]
+
+    def run(streams):
+        xs = [to_dev(x) for x in x_T]
+        torch.cuda.synchronize()
+        for st, cond, s in zip(states, conds, streams):
+            st.reset(s)
+            st.set_cond(cond, s)
+        for k, q in enumerate(quotas):
+            for st, x, s in zip(states, xs, streams):
+                st.cached_step(x, times[k], times[k + 1], q, s)
+        torch.cuda.synchronize()
+        return [x.cpu() for x in xs]
+
+    say("two states, one stream")
+    one = torch.cuda.current_stream().cuda_stream
+    seq = run([one, one])
+    say("two states, two streams")
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    par = run([s1.cuda_stream, s2.cuda_stream])
+    assert all(torch.equal(a, b) for a, b in zip(seq, par))
+    assert not torch.equal(seq[0], seq[1])
+
+
 def test_trellis16_cached_step_full_depth(torch):
     """Full-size model (24 blocks, width 1024, 4096 tokens), cached step at 80% quota."""
     cfg = synth.TRELLIS16
