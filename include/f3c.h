@@ -25,6 +25,12 @@
  * therefore step concurrently on different streams. Calls on one state must
  * be ordered, normally by issuing them on one stream.
  *
+ * Graph capture: f3c_state_reset, f3c_set_cond, f3c_set_uncond and the step
+ * calls enqueue kernels only (no allocation, memset node, host copy or
+ * synchronisation), so a caller may capture them in a HIP graph. The graph
+ * replays the pointers and sizes of the capture: the quotas and step times
+ * are fixed at capture time.
+ *
  * Layouts: latent grids and velocities are float32 [B][N][8], token-major,
  * with token n = (z*G + y)*G + x for an G x G x G grid (the flatten order of
  * the D x H x W latent, Sec. 4.2). Condition tokens are float32 [B][Nc][dc].
@@ -126,7 +132,9 @@ int f3c_state_bytes_ex(const f3c_model* m, int32_t batch, uint32_t flags, size_t
 int f3c_state_create_ex(f3c_model* m, int32_t batch, uint32_t flags, void* state_dev, size_t bytes,
                         f3c_stream stream, f3c_state** out);
 
-/* Zero both velocity caches (start of a new trajectory). */
+/* Zero both velocity caches (start of a new trajectory). Done by a kernel, not
+ * a memset, so that a whole trajectory (reset, f3c_set_cond, steps) can be
+ * captured in one HIP graph and replayed. */
 int f3c_state_reset(f3c_state* s, f3c_stream stream);
 
 /* SSC weight omega of Eq. (6), in [0, 1]. */

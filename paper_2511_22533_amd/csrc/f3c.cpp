@@ -564,8 +564,8 @@ int f3c_state_create_ex(f3c_model* m, int32_t batch, uint32_t flags, void* state
   s->ws = (float*)take(kAttnWsBytes);
   s->ws_bytes = kAttnWsBytes;
   hipStream_t st = (hipStream_t)stream;
-  hipError_t e = hipMemsetAsync(s->v[0], 0, R * 32, st);
-  if (e == hipSuccess) e = hipMemsetAsync(s->v[1], 0, R * 32, st);
+  hipError_t e = f3c::launch_zero(s->v[0], R * 32, st);
+  if (e == hipSuccess) e = f3c::launch_zero(s->v[1], R * 32, st);
   if (e != hipSuccess) {
     delete s;
     return fail(F3C_EHIP, "zeroing caches: %s", hipGetErrorString(e));
@@ -590,8 +590,8 @@ void f3c_state_destroy(f3c_state* s) {
 int f3c_state_reset(f3c_state* s, f3c_stream stream) {
   if (!s) return fail(F3C_EINVAL, "state is NULL");
   const size_t R = (size_t)s->B * s->m->N;
-  HIP_TRY(hipMemsetAsync(s->v[0], 0, R * 32, (hipStream_t)stream));
-  HIP_TRY(hipMemsetAsync(s->v[1], 0, R * 32, (hipStream_t)stream));
+  HIP_TRY(f3c::launch_zero(s->v[0], R * 32, (hipStream_t)stream));
+  HIP_TRY(f3c::launch_zero(s->v[1], R * 32, (hipStream_t)stream));
   s->cur = 0;
   return F3C_OK;
 }

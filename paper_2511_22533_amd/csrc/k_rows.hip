@@ -3,6 +3,8 @@
 // projection, merge + Euler + cache rotation, the timestep/modulation GEMVs
 // and dtype conversion. All are HBM/latency bound; one 64-wide wavefront owns a
 // row and lanes stride across the row so every load instruction is coalesced.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -356,6 +358,22 @@ hipError_t launch_final(int dt, const float* h, int rows, int d, const void* w_o
   dim3 grid((rows + 3) / 4);
   if (dt == DT_BF16) F3C_NPL_LAUNCH(d, k_final, bf16, grid, s, h, rows, (const bf16*)w_out, b_out, v_act);
   F3C_NPL_LAUNCH(d, k_final, float, grid, s, h, rows, (const float*)w_out, b_out, v_act);
+}
+
+// Zero fill with 16-byte stores: a kernel rather than a memset node, so that a
+// caller may capture the state reset in a graph.
+__global__ __launch_bounds__(256) void k_zero16(u32x4* __restrict__ p, int64_t n16) {
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += stride) p[i] = u32x4{0, 0, 0, 0};
+}
+
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t s) {
+  if (bytes % 16 || (uintptr_t)p % 16) return hipErrorInvalidValue;
+  const int64_t n16 = (int64_t)(bytes / 16);
+  if (n16 == 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((n16 + 255) / 256, 2048);
+  launch(k_zero16, dim3((unsigned)blocks), dim3(256), 0, s, reinterpret_cast<u32x4*>(p), n16);
+  return hipGetLastError();
 }
 
 hipError_t launch_euler(float* x, const float* v_cache, const float* v_act, const float* v_unc, float ga, float gw,

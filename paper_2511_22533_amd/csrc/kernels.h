@@ -46,6 +46,9 @@ hipError_t launch_ln_mod(int dt, const float* h, int rows, int d, const float* s
 hipError_t launch_final(int dt, const float* h, int rows, int d, const void* w_out, const float* b_out,
                         float* v_act, hipStream_t s);
 
+// Zero bytes (a multiple of 16) at p (16-byte aligned) with a kernel.
+hipError_t launch_zero(void* p, size_t bytes, hipStream_t s);
+
 // Merge + Euler + rotate: v = (pos >= 0 ? v_act[pos] : v_cache); x -= dt * v; v_new = v.
 // pos == nullptr means every token active at row act.off[b] + i. With v_unc (guided step), an
 // active row's v is ga * v_act[p] - gw * v_unc[p], each operation rounded.

@@ -217,6 +217,55 @@ def test_two_states_on_two_streams_match_sequential(torch):
     assert not torch.equal(seq[0], seq[1])
 
 
+def test_graph_capture_of_a_trajectory_replays_exactly(torch):
+    """A whole trajectory (state reset, condition K/V, cached steps) captured
+    in one HIP graph: the library records only kernels on the caller's stream
+    (the reset zeroes the caches with a kernel, not a memset node), so every
+    replay, with eager work and synchronisations in between, gives the eager
+    trajectory bit for bit."""
+    from paper_2511_22533_amd import f3c
+    cfg = depth_variant(synth.TRELLIS16, 2)
+    model = f3c.Model(cfg).load(synth.make_weights(cfg, seed=0))
+    state = f3c.State(model, 1)
+    cond = to_dev(synth.make_cond(cfg, 1))
+    x_T = to_dev(synth.make_noise(cfg, 1))
+    times = schedule.time_grid(6, 3.0)
+    quotas = [[0], [0], [1024], [2048], [3000], [3276]]
+
+    def trajectory(x):
+        state.reset()
+        state.set_cond(cond)
+        for k, q in enumerate(quotas):
+            state.cached_step(x, times[k], times[k + 1], q)
+
+    x = x_T.clone()
+    say("eager trajectory")
+    trajectory(x)
+    torch.cuda.synchronize()
+    eager = x.clone()
+    xg = x_T.clone()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    say("capture")
+    with torch.cuda.graph(graph):
+        trajectory(xg)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        xg.copy_(x_T)
+        junk = torch.arange(1 << 20, device="cuda", dtype=torch.float32).mul_(0.5).sum()
+        torch.cuda.synchronize()
+        say("replay", rep)
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(xg, eager), f"replay {rep}"
+        assert float(junk) > 0
+    # the eager path still works after capture, and still agrees
+    x2 = x_T.clone()
+    trajectory(x2)
+    torch.cuda.synchronize()
+    assert torch.equal(x2, eager)
+
+
 def test_trellis16_cached_step_full_depth(torch):
     """Full-size model (24 blocks, width 1024, 4096 tokens), cached step at 80% quota."""
     cfg = synth.TRELLIS16
