@@ -9,6 +9,7 @@
 #include <cstdio>
 #include <cstring>
 #include <string>
+#include <unordered_map>
 #include <vector>
 
 #include "../../include/f3c.h"
@@ -66,13 +67,14 @@ struct f3c_model {
   bool loaded = false;
   // group bases (bytes)
   size_t mod_w, mod_b, kv_w, kv_b;
+  // Byte offsets of the other weights, resolved from their names once at
+  // creation so that a step does no name lookups.
+  struct Top { size_t in_w, in_b, pos, t1_w, t1_b, t2_w, t2_b, out_w, out_b; } top{};
+  struct Block { size_t qkv_w, qkv_b, o_w, o_b, q_w, q_b, co_w, co_b, fc1_w, fc1_b, fc2_w, fc2_b; };
+  std::vector<Block> blk;
 
-  const void* w(const std::string& name) const {
-    for (const auto& s : specs)
-      if (s.name == name) return wdev + s.off;
-    return nullptr;
-  }
-  const float* b(const std::string& name) const { return static_cast<const float*>(w(name)); }
+  const void* w(size_t off) const { return wdev + off; }
+  const float* b(size_t off) const { return reinterpret_cast<const float*>(wdev + off); }
 };
 
 struct Prof {
@@ -243,14 +245,14 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
   {
     Scope sc(s, F3C_PROF_MOD, st, 0, (double)es * d * (256 + d + 6.0 * L * d));
     const char* mw = m->wdev;
-    HIP_TRY(launch_gemv(dt, m->w("t1_w"), m->b("t1_b"), nullptr, t, GEMV_IN_TIMESTEP, 1, d, 256, s->temb, st));
-    HIP_TRY(launch_gemv(dt, m->w("t2_w"), m->b("t2_b"), s->temb, 0.0, GEMV_IN_PLAIN, 0, d, d, s->temb + d, st));
+    HIP_TRY(launch_gemv(dt, m->w(m->top.t1_w), m->b(m->top.t1_b), nullptr, t, GEMV_IN_TIMESTEP, 1, d, 256, s->temb, st));
+    HIP_TRY(launch_gemv(dt, m->w(m->top.t2_w), m->b(m->top.t2_b), s->temb, 0.0, GEMV_IN_PLAIN, 0, d, d, s->temb + d, st));
     HIP_TRY(launch_gemv_t(dt, mw + m->mod_w, (const float*)(mw + m->mod_b), s->temb + d, 6 * L * d, d, s->mod, st));
   }
   if (arows > 0) {
     {
       Scope sc(s, F3C_PROF_EMBED, st, 0, arows * (32.0 + d * es + P * d * 4.0));
-      HIP_TRY(launch_embed(dt, x, N, idx, act, m->w("in_w"), m->b("in_b"), m->w("pos"), d, s->h, guide ? arows : 0,
+      HIP_TRY(launch_embed(dt, x, N, idx, act, m->w(m->top.in_w), m->b(m->top.in_b), m->w(m->top.pos), d, s->h, guide ? arows : 0,
                            st));
     }
     const int dm = m->dm;
@@ -266,7 +268,7 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
     const size_t hslice = (size_t)rows * d;       // trace size checked by step_common
     if (s->trace) HIP_TRY(hipMemcpyAsync(s->trace, s->h, hslice * 4, hipMemcpyDeviceToDevice, st));
     for (int l = 0; l < L; ++l) {
-      const std::string p = "blk" + std::to_string(l) + ".";
+      const f3c_model::Block& bw = m->blk[l];
       const float* md = s->mod + (size_t)l * 6 * d;
       {
         Scope sc(s, F3C_PROF_LN, st, 0, lnb);
@@ -274,7 +276,7 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
       }
       {
         Scope sc(s, F3C_PROF_GEMM_QKV, st, 2.0 * rows * 3 * d * d, proj_bytes(3 * dd, dd, false));
-        HIP_TRY(launch_gemm(SITE_QKV, dt, EPI_STORE, rows, 3 * d, d, s->u, d, m->w(p + "qkv_w"), d, m->b(p + "qkv_b"),
+        HIP_TRY(launch_gemm(SITE_QKV, dt, EPI_STORE, rows, 3 * d, d, s->u, d, m->w(bw.qkv_w), d, m->b(bw.qkv_b),
                             nullptr, s->qkv, 3 * d, nullptr, 0, st));
       }
       {
@@ -288,7 +290,7 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
       }
       {
         Scope sc(s, F3C_PROF_GEMM_O, st, 2.0 * rows * d * d, proj_bytes(dd, dd, true));
-        HIP_TRY(launch_gemm(SITE_O, dt, EPI_RESID, rows, d, d, s->att, d, m->w(p + "o_w"), d, m->b(p + "o_b"), md + 2 * d,
+        HIP_TRY(launch_gemm(SITE_O, dt, EPI_RESID, rows, d, d, s->att, d, m->w(bw.o_w), d, m->b(bw.o_b), md + 2 * d,
                             nullptr, 0, s->h, d, st));
       }
       {
@@ -297,7 +299,7 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
       }
       {
         Scope sc(s, F3C_PROF_GEMM_Q, st, 2.0 * rows * d * d, proj_bytes(dd, dd, false));
-        HIP_TRY(launch_gemm(SITE_Q, dt, EPI_STORE, rows, d, d, s->u, d, m->w(p + "q_w"), d, m->b(p + "q_b"), nullptr,
+        HIP_TRY(launch_gemm(SITE_Q, dt, EPI_STORE, rows, d, d, s->u, d, m->w(bw.q_w), d, m->b(bw.q_b), nullptr,
                             s->qc, d, nullptr, 0, st));
       }
       {
@@ -308,7 +310,7 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
       }
       {
         Scope sc(s, F3C_PROF_GEMM_CO, st, 2.0 * rows * d * d, proj_bytes(dd, dd, true));
-        HIP_TRY(launch_gemm(SITE_CO, dt, EPI_RESID, rows, d, d, s->att, d, m->w(p + "co_w"), d, m->b(p + "co_b"), nullptr,
+        HIP_TRY(launch_gemm(SITE_CO, dt, EPI_RESID, rows, d, d, s->att, d, m->w(bw.co_w), d, m->b(bw.co_b), nullptr,
                             nullptr, 0, s->h, d, st));
       }
       {
@@ -317,12 +319,12 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
       }
       {
         Scope sc(s, F3C_PROF_GEMM_FC1, st, 2.0 * rows * dm * d, proj_bytes(dm, dd, false));
-        HIP_TRY(launch_gemm(SITE_FC1, dt, EPI_GELU, rows, dm, d, s->u, d, m->w(p + "fc1_w"), d, m->b(p + "fc1_b"), nullptr,
+        HIP_TRY(launch_gemm(SITE_FC1, dt, EPI_GELU, rows, dm, d, s->u, d, m->w(bw.fc1_w), d, m->b(bw.fc1_b), nullptr,
                             s->hid, dm, nullptr, 0, st));
       }
       {
         Scope sc(s, F3C_PROF_GEMM_FC2, st, 2.0 * rows * d * dm, proj_bytes(dd, dm, true));
-        HIP_TRY(launch_gemm(SITE_FC2, dt, EPI_RESID, rows, d, dm, s->hid, dm, m->w(p + "fc2_w"), dm, m->b(p + "fc2_b"),
+        HIP_TRY(launch_gemm(SITE_FC2, dt, EPI_RESID, rows, d, dm, s->hid, dm, m->w(bw.fc2_w), dm, m->b(bw.fc2_b),
                             md + 5 * d, nullptr, 0, s->h, d, st));
       }
       if (s->trace)
@@ -330,7 +332,7 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
     }
     {
       Scope sc(s, F3C_PROF_FINAL, st, 0, rows * (d * 4.0 + 32));
-      HIP_TRY(launch_final(dt, s->h, rows, d, m->w("out_w"), m->b("out_b"), s->vact, st));
+      HIP_TRY(launch_final(dt, s->h, rows, d, m->w(m->top.out_w), m->b(m->top.out_b), s->vact, st));
     }
   }
   {
@@ -423,6 +425,16 @@ int f3c_model_create(const f3c_model_cfg* cfg, f3c_model** out) {
     off = align256(off + bytes_of(s));
   }
   m->wbytes = off;
+  std::unordered_map<std::string, size_t> at;
+  for (const auto& s : m->specs) at.emplace(s.name, s.off);
+  m->top = {at.at("in_w"), at.at("in_b"), at.at("pos"), at.at("t1_w"), at.at("t1_b"),
+            at.at("t2_w"), at.at("t2_b"), at.at("out_w"), at.at("out_b")};
+  for (int l = 0; l < L; ++l) {
+    const std::string p = "blk" + std::to_string(l) + ".";
+    m->blk.push_back({at.at(p + "qkv_w"), at.at(p + "qkv_b"), at.at(p + "o_w"), at.at(p + "o_b"), at.at(p + "q_w"),
+                      at.at(p + "q_b"), at.at(p + "co_w"), at.at(p + "co_b"), at.at(p + "fc1_w"), at.at(p + "fc1_b"),
+                      at.at(p + "fc2_w"), at.at(p + "fc2_b")});
+  }
   *out = m;
   return F3C_OK;
 }
@@ -855,8 +867,8 @@ int f3c_op_modulation(const f3c_model* m, double t, float* mod_dev, float* scrat
   if (!std::isfinite(t)) return fail(F3C_EINVAL, "t must be finite");
   hipStream_t st = (hipStream_t)stream;
   const int d = m->d, dt = m->cfg.dtype;
-  HIP_TRY(launch_gemv(dt, m->w("t1_w"), m->b("t1_b"), nullptr, t, GEMV_IN_TIMESTEP, 1, d, 256, scratch_dev, st));
-  HIP_TRY(launch_gemv(dt, m->w("t2_w"), m->b("t2_b"), scratch_dev, 0.0, GEMV_IN_PLAIN, 0, d, d, scratch_dev + d, st));
+  HIP_TRY(launch_gemv(dt, m->w(m->top.t1_w), m->b(m->top.t1_b), nullptr, t, GEMV_IN_TIMESTEP, 1, d, 256, scratch_dev, st));
+  HIP_TRY(launch_gemv(dt, m->w(m->top.t2_w), m->b(m->top.t2_b), scratch_dev, 0.0, GEMV_IN_PLAIN, 0, d, d, scratch_dev + d, st));
   HIP_TRY(launch_gemv_t(dt, m->wdev + m->mod_w, (const float*)(m->wdev + m->mod_b), scratch_dev + d, 6 * m->L * d, d,
                         mod_dev, st));
   return F3C_OK;
@@ -886,7 +898,7 @@ int f3c_op_embed(const f3c_model* m, int32_t batch, const float* x, const int32_
   if (!idx_active)
     for (int b = 0; b < batch; ++b)
       if (act.off[b + 1] - act.off[b] != m->N) return fail(F3C_EINVAL, "without idx_active every token is active");
-  HIP_TRY(launch_embed(m->cfg.dtype, x, m->N, idx_active, act, m->w("in_w"), m->b("in_b"), m->w("pos"), m->d, h,
+  HIP_TRY(launch_embed(m->cfg.dtype, x, m->N, idx_active, act, m->w(m->top.in_w), m->b(m->top.in_b), m->w(m->top.pos), m->d, h,
                        0, (hipStream_t)stream));
   return F3C_OK;
 }
@@ -894,7 +906,7 @@ int f3c_op_embed(const f3c_model* m, int32_t batch, const float* x, const int32_
 int f3c_op_final(const f3c_model* m, int32_t rows, const float* h, float* v_act, f3c_stream stream) {
   if (!m || !h || !v_act || rows < 0) return fail(F3C_EINVAL, "bad argument");
   if (!m->loaded) return fail(F3C_ESTATE, "weights not loaded");
-  HIP_TRY(launch_final(m->cfg.dtype, h, rows, m->d, m->w("out_w"), m->b("out_b"), v_act, (hipStream_t)stream));
+  HIP_TRY(launch_final(m->cfg.dtype, h, rows, m->d, m->w(m->top.out_w), m->b(m->top.out_b), v_act, (hipStream_t)stream));
   return F3C_OK;
 }
 
