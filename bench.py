@@ -11,8 +11,9 @@ A "step" is one denoising step of that schedule: stability scoring and top-k
 selection, gather + embedding, timestep modulation, 24 blocks on the active
 tokens, output projection and the merge/Euler/cache update. K timed steps walk
 through the schedule and wrap around; every trajectory start re-zeroes the
-caches, reloads x_T and recomputes the condition keys/values inside the timed
-region.
+caches, reloads x_T, recomputes the condition keys/values and plans the
+timestep modulation of all the trajectory's step times (one pass over the
+modulation weights per 8 times) inside the timed region.
 
 Prints one JSON line. ``value`` is denoising steps per second; the line also
 carries active tokens/s, the whole-step MFMA fraction (FLOPs model of the
@@ -322,6 +323,7 @@ def main():
             state.set_cond(cond_dev)
             if uncond_dev is not None:
                 state.set_uncond(uncond_dev)
+            state.plan_times(times[:-1])
         q = quotas[k].tolist()
         if guided[k]:
             state.guided_step(x, float(times[k]), float(times[k + 1]), q if any(q) else None, w.guidance)

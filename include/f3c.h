@@ -25,11 +25,11 @@
  * therefore step concurrently on different streams. Calls on one state must
  * be ordered, normally by issuing them on one stream.
  *
- * Graph capture: f3c_state_reset, f3c_set_cond, f3c_set_uncond and the step
- * calls enqueue kernels only (no allocation, memset node, host copy or
- * synchronisation), so a caller may capture them in a HIP graph. The graph
- * replays the pointers and sizes of the capture: the quotas and step times
- * are fixed at capture time.
+ * Graph capture: f3c_state_reset, f3c_set_cond, f3c_set_uncond,
+ * f3c_state_plan_times and the step calls enqueue kernels only (no
+ * allocation, memset node, host copy or synchronisation), so a caller may
+ * capture them in a HIP graph. The graph replays the pointers and sizes of the
+ * capture: the quotas and step times are fixed at capture time.
  *
  * Layouts: latent grids and velocities are float32 [B][N][8], token-major,
  * with token n = (z*G + y)*G + x for an G x G x G grid (the flatten order of
@@ -57,6 +57,7 @@ extern "C" {
 #define F3C_MAX_BATCH 64
 #define F3C_STATE_GUIDED 1u   /* state flag: room for guided steps (two passes per sample) */
 #define F3C_MAX_TOKENS 32768
+#define F3C_MAX_PLAN 1024   /* times one modulation plan may hold */
 
 typedef void* f3c_stream; /* hipStream_t */
 
@@ -150,6 +151,28 @@ int f3c_set_cond(f3c_state* s, const float* cond_dev, f3c_stream stream);
  * f3c_set_cond into the second half of the keys/values. Needs a state created
  * with F3C_STATE_GUIDED (else F3C_ESTATE). */
 int f3c_set_uncond(f3c_state* s, const float* uncond_dev, f3c_stream stream);
+
+/* Modulation plan. The timestep modulation of every block (the time embedding
+ * followed by the 6*width adaLN vector of each block) depends only on t and
+ * the weights. f3c_state_plan_times computes it for the n times t_host[0..n-1]
+ * (normally the trajectory's time grid) in ceil(n / 8) passes over the
+ * modulation weights, instead of one pass per step, into the caller's device
+ * buffer plan_dev (256-byte aligned, at least f3c_plan_bytes(m, n) bytes):
+ * float32 [n][L][6][width] followed by [n][2][width] of time-embedding scratch.
+ * A later step of this state whose t equals one of those times exactly reads
+ * the planned vector; any other t computes its own as before. The planned
+ * vectors are bit-identical to the ones a step computes, so planning does not
+ * change results. The buffer must stay alive, and the weights unchanged, while
+ * the plan is in use; calling again replaces the plan, n == 0 clears it
+ * (plan_dev may then be NULL), and f3c_state_reset keeps it. The work is
+ * enqueued on stream; steps on another stream must be ordered after it.
+ * Errors: F3C_EINVAL (n outside 0..F3C_MAX_PLAN, a non-finite time, NULL or
+ * misaligned buffer), F3C_ENOMEM (buffer too small), F3C_ESTATE (weights not
+ * loaded); the previous plan is then kept. After F3C_EHIP (a launch failed)
+ * the state has no plan. */
+int f3c_plan_bytes(const f3c_model* m, int32_t n, size_t* bytes);
+int f3c_state_plan_times(f3c_state* s, const double* t_host, int32_t n, void* plan_dev, size_t bytes,
+                         f3c_stream stream);
 
 /* One denoising step of Algorithm 1 with every token active (Phase 1, Phase 3
  * correction steps): v = G(x_t, t, c); x <- x - (t - t_next) v; caches rotate.

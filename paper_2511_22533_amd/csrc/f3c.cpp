@@ -4,6 +4,7 @@
 // L blocks on the compacted set -> final projection -> merge/Euler/rotate.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -96,6 +97,8 @@ struct f3c_state {
   float* ws = nullptr;          // attention key-split partials
   size_t ws_bytes = 0;
   bool guided = false;          // activations and condition K/V sized for two passes per sample
+  std::vector<double> plan_t;   // times of the modulation plan, [i] at plan_mod + i * L * 6d
+  float* plan_mod = nullptr;
   float* trace = nullptr;       // debug: residual stream after the embedding and after each block
   size_t trace_bytes = 0;
   bool cond_set = false, uncond_set = false, record_scores = false;
@@ -242,7 +245,13 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
     idx = s->idx;
     pos = s->pos;
   }
-  {
+  const float* mod = s->mod;
+  int planned = -1;
+  for (size_t i = 0; i < s->plan_t.size() && planned < 0; ++i)
+    if (s->plan_t[i] == t) planned = (int)i;
+  if (planned >= 0) {
+    mod = s->plan_mod + (size_t)planned * 6 * L * d;
+  } else {
     Scope sc(s, F3C_PROF_MOD, st, 0, (double)es * d * (256 + d + 6.0 * L * d));
     const char* mw = m->wdev;
     HIP_TRY(launch_gemv(dt, m->w(m->top.t1_w), m->b(m->top.t1_b), nullptr, t, GEMV_IN_TIMESTEP, 1, d, 256, s->temb, st));
@@ -269,7 +278,7 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
     if (s->trace) HIP_TRY(hipMemcpyAsync(s->trace, s->h, hslice * 4, hipMemcpyDeviceToDevice, st));
     for (int l = 0; l < L; ++l) {
       const f3c_model::Block& bw = m->blk[l];
-      const float* md = s->mod + (size_t)l * 6 * d;
+      const float* md = mod + (size_t)l * 6 * d;
       {
         Scope sc(s, F3C_PROF_LN, st, 0, lnb);
         HIP_TRY(launch_ln_mod(dt, s->h, rows, d, md, md + d, s->u, st));
@@ -649,6 +658,56 @@ int f3c_set_uncond(f3c_state* s, const float* uncond_dev, f3c_stream stream) {
   if (!uncond_dev) return fail(F3C_EINVAL, "uncond is NULL");
   if ((rc = cond_kv(s, uncond_dev, 1, (hipStream_t)stream))) return rc;
   s->uncond_set = true;
+  return F3C_OK;
+}
+
+int f3c_plan_bytes(const f3c_model* m, int32_t n, size_t* bytes) {
+  if (!m || !bytes) return fail(F3C_EINVAL, "NULL argument");
+  if (n < 0 || n > F3C_MAX_PLAN) return fail(F3C_EINVAL, "plan of %d times outside 0..%d", n, F3C_MAX_PLAN);
+  *bytes = align256((size_t)n * 6 * m->L * m->d * 4) + align256((size_t)n * 2 * m->d * 4);
+  return F3C_OK;
+}
+
+int f3c_state_plan_times(f3c_state* s, const double* t_host, int32_t n, void* plan_dev, size_t bytes,
+                         f3c_stream stream) {
+  int rc = check_state(s);
+  if (rc) return rc;
+  size_t need = 0;
+  if ((rc = f3c_plan_bytes(s->m, n, &need))) return rc;
+  if (n == 0) {
+    s->plan_t.clear();
+    s->plan_mod = nullptr;
+    return F3C_OK;
+  }
+  if (!t_host || !plan_dev) return fail(F3C_EINVAL, "NULL argument");
+  for (int32_t i = 0; i < n; ++i)
+    if (!std::isfinite(t_host[i])) return fail(F3C_EINVAL, "plan time %d is not finite", i);
+  if ((uintptr_t)plan_dev & 255) return fail(F3C_EINVAL, "plan buffer must be 256-byte aligned");
+  if (bytes < need) return fail(F3C_ENOMEM, "plan buffer %zu < %zu bytes", bytes, need);
+  f3c_model* m = s->m;
+  const int d = m->d, L = m->L, dt = m->cfg.dtype, R = 6 * L * d;
+  const size_t es = m->es;
+  float* mod = static_cast<float*>(plan_dev);
+  float* temb = reinterpret_cast<float*>(static_cast<char*>(plan_dev) + align256((size_t)n * R * 4));
+  hipStream_t st = (hipStream_t)stream;
+  s->plan_t.clear();                     // no step may read a half-enqueued plan
+  s->plan_mod = nullptr;
+  {
+    const int passes = (n + 7) / 8;
+    Scope sc(s, F3C_PROF_MOD, st, 0, (double)es * d * ((256.0 + d) * n + (double)R * passes));
+    const char* mw = m->wdev;
+    for (int32_t i = 0; i < n; ++i) {
+      float* e = temb + (size_t)i * 2 * d;
+      HIP_TRY(launch_gemv(dt, m->w(m->top.t1_w), m->b(m->top.t1_b), nullptr, t_host[i], GEMV_IN_TIMESTEP, 1, d, 256, e,
+                          st));
+      HIP_TRY(launch_gemv(dt, m->w(m->top.t2_w), m->b(m->top.t2_b), e, 0.0, GEMV_IN_PLAIN, 0, d, d, e + d, st));
+    }
+    for (int32_t c = 0; c < n; c += 8)
+      HIP_TRY(launch_gemv_tn(dt, mw + m->mod_w, (const float*)(mw + m->mod_b), temb + (size_t)c * 2 * d + d, 2 * d,
+                             std::min(8, n - c), R, d, mod + (size_t)c * R, R, st));
+  }
+  s->plan_t.assign(t_host, t_host + n);
+  s->plan_mod = mod;
   return F3C_OK;
 }
 

@@ -200,6 +200,11 @@ int main(int argc, char** argv) {
   std::vector<double> times(steps + 1);
   check(f3c_time_grid(steps, eta, times.data()), "f3c_time_grid");
   std::vector<int32_t> qb(batch);
+  // The modulation of every step time, planned at each trajectory start.
+  size_t pbytes = 0;
+  check(f3c_plan_bytes(m, steps, &pbytes), "f3c_plan_bytes");
+  void* plan = nullptr;
+  hip_check(hipMalloc(&plan, pbytes), "hipMalloc plan");
 
   auto run_steps = [&]() {
     for (int k = 0; k < steps; ++k) {
@@ -214,6 +219,7 @@ int main(int argc, char** argv) {
   hipGraphExec_t gexec = nullptr;
   if (use_graph) {
     check(f3c_set_cond(s, cond, st), "f3c_set_cond");    // the steps check that a condition is set
+    check(f3c_state_plan_times(s, times.data(), steps, plan, pbytes, st), "f3c_state_plan_times");
     hip_check(hipStreamSynchronize(st), "hipStreamSynchronize");
     hipGraph_t graph;
     hip_check(hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal), "hipStreamBeginCapture");
@@ -232,6 +238,7 @@ int main(int argc, char** argv) {
     check(f3c_state_reset(s, st), "f3c_state_reset");
     hip_check(hipMemcpyAsync(x, x0, nx * 4, hipMemcpyDeviceToDevice, st), "hipMemcpyAsync");
     check(f3c_set_cond(s, cond, st), "f3c_set_cond");
+    check(f3c_state_plan_times(s, times.data(), steps, plan, pbytes, st), "f3c_state_plan_times");
     if (use_graph) hip_check(hipGraphLaunch(gexec, st), "hipGraphLaunch");
     else run_steps();
   }
@@ -250,6 +257,7 @@ int main(int argc, char** argv) {
   hip_check(hipFree(x0), "hipFree");
   hip_check(hipFree(x), "hipFree");
   hip_check(hipFree(cond), "hipFree");
+  hip_check(hipFree(plan), "hipFree");
   hip_check(hipFree(sdev), "hipFree");
   hip_check(hipFree(wdev), "hipFree");
   hip_check(hipStreamDestroy(st), "hipStreamDestroy");

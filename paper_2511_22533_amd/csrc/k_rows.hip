@@ -217,6 +217,7 @@ __global__ __launch_bounds__(256) void k_euler(float* __restrict__ x, const floa
 // then spans 256 workgroups instead of a few waves walking rows one after the
 // other at HBM latency each.
 constexpr int kGemvRowsPerWave = 1;
+constexpr int kGemvChunk = 8;               // times per pass of the batched modulation
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_gemv(const T* __restrict__ W, const float* __restrict__ bias,
@@ -308,6 +309,74 @@ __global__ __launch_bounds__(256) void k_gemv_t(const T* __restrict__ Wt, const 
 #pragma unroll
     for (int e = 0; e < V; ++e)
       y[r0 + e] = ((acc[e] + part[0][lane * V + e]) + (part[1][lane * V + e] + part[2][lane * V + e])) + bias[r0 + e];
+  }
+}
+
+// The all-block modulation for up to kGemvChunk times in one pass over the
+// input-major weight: each 16-byte weight load serves every time of the chunk.
+// Per output the operations and their order are those of k_gemv_t (four
+// sequential K quarters, combined as ((q0 + q1) + (q2 + q3)) + bias), so each
+// time's result equals k_gemv_t's bit for bit. Rows of xs past nt are zero and
+// their results are not stored.
+template <typename T>
+__global__ __launch_bounds__(256) void k_gemv_tn(const T* __restrict__ Wt, const float* __restrict__ bias,
+                                                 const float* __restrict__ x, int ldx, int nt, int R, int K,
+                                                 float* __restrict__ y, int ldy) {
+  constexpr int V = 16 / sizeof(T), NT = kGemvChunk;
+  __shared__ float part[3][64 * V];
+  extern __shared__ float xs[];                     // [NT][K]
+  for (int j = threadIdx.x; j < NT * K; j += 256) {
+    const int i = j / K, k = j - i * K;
+    xs[j] = i < nt ? silu(x[(size_t)i * ldx + k]) : 0.0f;
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r0 = blockIdx.x * 64 * V + lane * V;
+  const int kq = K / 4, k0 = wave * kq;
+  float acc[NT][V];
+#pragma unroll
+  for (int i = 0; i < NT; ++i)
+#pragma unroll
+    for (int e = 0; e < V; ++e) acc[i][e] = 0.0f;
+  if (r0 < R) {
+    const T* w = Wt + (size_t)k0 * R + r0;
+#pragma unroll 4
+    for (int k = 0; k < kq; ++k) {
+      float wf[V];
+      if constexpr (sizeof(T) == 2) {
+        const bf16x8 wv = *reinterpret_cast<const bf16x8*>(w + (size_t)k * R);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) wf[e] = (float)wv[e];
+      } else {
+        const float4 wv = *reinterpret_cast<const float4*>(w + (size_t)k * R);
+        wf[0] = wv.x;
+        wf[1] = wv.y;
+        wf[2] = wv.z;
+        wf[3] = wv.w;
+      }
+#pragma unroll
+      for (int i = 0; i < NT; ++i) {
+        const float xv = xs[i * K + k0 + k];
+#pragma unroll
+        for (int e = 0; e < V; ++e) acc[i][e] += wf[e] * xv;
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < NT; ++i) {
+    if (i >= nt) break;                             // nt is uniform: every wave takes every barrier
+    if (wave > 0) {
+#pragma unroll
+      for (int e = 0; e < V; ++e) part[wave - 1][lane * V + e] = acc[i][e];
+    }
+    __syncthreads();
+    if (wave == 0 && r0 < R) {
+#pragma unroll
+      for (int e = 0; e < V; ++e)
+        y[(size_t)i * ldy + r0 + e] =
+            ((acc[i][e] + part[0][lane * V + e]) + (part[1][lane * V + e] + part[2][lane * V + e])) + bias[r0 + e];
+    }
+    __syncthreads();
   }
 }
 
@@ -407,6 +476,19 @@ hipError_t launch_gemv_t(int dt, const void* Wt, const float* bias, const float*
     launch(k_gemv_t<bf16>, grid, dim3(256), 0, s, (const bf16*)Wt, bias, x, R, K, y);
   else
     launch(k_gemv_t<float>, grid, dim3(256), 0, s, (const float*)Wt, bias, x, R, K, y);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemv_tn(int dt, const void* Wt, const float* bias, const float* x, int ldx, int nt, int R, int K,
+                          float* y, int ldy, hipStream_t s) {
+  if (nt < 1 || nt > kGemvChunk || K % 4) return hipErrorInvalidValue;
+  const int per_block = 64 * (dt == DT_BF16 ? 8 : 4);
+  dim3 grid((R + per_block - 1) / per_block);
+  const size_t lds = (size_t)kGemvChunk * K * sizeof(float);
+  if (dt == DT_BF16)
+    launch(k_gemv_tn<bf16>, grid, dim3(256), lds, s, (const bf16*)Wt, bias, x, ldx, nt, R, K, y, ldy);
+  else
+    launch(k_gemv_tn<float>, grid, dim3(256), lds, s, (const float*)Wt, bias, x, ldx, nt, R, K, y, ldy);
   return hipGetLastError();
 }
 

@@ -66,6 +66,9 @@ hipError_t launch_gemv(int dt, const void* W, const float* bias, const float* x,
 // (Wt [K][R]); R a multiple of 16 / sizeof(element), K a multiple of 4, K <= 4096.
 hipError_t launch_gemv_t(int dt, const void* Wt, const float* bias, const float* x, int R, int K, float* y,
                          hipStream_t s);
+// Up to 8 times at once: x [nt][ldx] (each time's t2 output), y [nt][ldy].
+hipError_t launch_gemv_tn(int dt, const void* Wt, const float* bias, const float* x, int ldx, int nt, int R, int K,
+                          float* y, int ldy, hipStream_t s);
 
 // Element type conversion f32 -> model dtype.
 hipError_t launch_convert(int dt, const float* src, void* dst, int64_t n, hipStream_t s);

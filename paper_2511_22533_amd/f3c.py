@@ -59,6 +59,8 @@ _SIGS = {
     "f3c_state_bytes_ex": (c_int, [c_p, c_int, ctypes.c_uint32, ctypes.POINTER(c_sz)]),
     "f3c_state_create_ex": (c_int, [c_p, c_int, ctypes.c_uint32, c_p, c_sz, c_p, ctypes.POINTER(c_p)]),
     "f3c_set_uncond": (c_int, [c_p, c_p, c_p]),
+    "f3c_plan_bytes": (c_int, [c_p, c_int, ctypes.POINTER(c_sz)]),
+    "f3c_state_plan_times": (c_int, [c_p, P_d, c_int, c_p, c_sz, c_p]),
     "f3c_guided_step": (c_int, [c_p, c_p, c_d, c_d, P_i32, c_d, c_p]),
     "f3c_guidance_active": (c_int, [c_d, c_d, c_d]),
     "f3c_state_trace_blocks": (c_int, [c_p, c_p, c_sz]),
@@ -273,6 +275,7 @@ class State:
                                         _stream(stream), ctypes.byref(h)))
         self.h = h
         self.last_guided = False
+        self.plan_buf = None
 
     def reset(self, stream=None):
         check(lib().f3c_state_reset(self.h, _stream(stream)))
@@ -285,6 +288,23 @@ class State:
 
     def set_uncond(self, uncond, stream=None):
         check(lib().f3c_set_uncond(self.h, uncond.data_ptr(), _stream(stream)))
+
+    def plan_times(self, times: Sequence[float], stream=None):
+        """Plan the timestep modulation of these times (normally the trajectory's
+        time grid): later steps at exactly one of them read it instead of
+        recomputing it. An empty sequence clears the plan. The plan's device
+        buffer belongs to this object and is reused while it is large enough."""
+        import torch
+        t = [float(v) for v in times]
+        if not t:
+            check(lib().f3c_state_plan_times(self.h, None, 0, None, 0, _stream(stream)))
+            return
+        b = c_sz()
+        check(lib().f3c_plan_bytes(self.model.h, len(t), ctypes.byref(b)))
+        if self.plan_buf is None or self.plan_buf.numel() < b.value:
+            self.plan_buf = torch.empty(b.value, dtype=torch.uint8, device="cuda")
+        check(lib().f3c_state_plan_times(self.h, (c_d * len(t))(*t), len(t), self.plan_buf.data_ptr(),
+                                         self.plan_buf.numel(), _stream(stream)))
 
     def full_step(self, x, t: float, t_next: float, stream=None):
         check(lib().f3c_full_step(self.h, x.data_ptr(), t, t_next, _stream(stream)))

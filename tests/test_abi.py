@@ -92,6 +92,23 @@ def test_guided_state_bytes_and_limits(L):
     assert L.f3c_set_uncond(None, None, None) == f3c.F3C_EINVAL
 
 
+def test_modulation_plan_bytes_and_host_checks(L):
+    """Plan size: the trajectory's modulation vectors [n][L][6][width] and the
+    time-embedding scratch [n][2][width], each 256-byte aligned; a 25-step
+    plan of the 24-block width-1024 model holds 14.2 MiB."""
+    m = f3c.Model(synth.TRELLIS16)
+    b = ctypes.c_size_t()
+    assert L.f3c_plan_bytes(m.h, 25, ctypes.byref(b)) == 0
+    assert b.value == 25 * 24 * 6 * 1024 * 4 + 25 * 2 * 1024 * 4
+    assert L.f3c_plan_bytes(m.h, 0, ctypes.byref(b)) == 0 and b.value == 0
+    assert L.f3c_plan_bytes(m.h, 1, ctypes.byref(b)) == 0 and b.value == 147456 * 4 + 8192
+    assert L.f3c_plan_bytes(m.h, 1024, ctypes.byref(b)) == 0
+    assert L.f3c_plan_bytes(m.h, 1025, ctypes.byref(b)) == f3c.F3C_EINVAL
+    assert L.f3c_plan_bytes(m.h, -1, ctypes.byref(b)) == f3c.F3C_EINVAL
+    assert L.f3c_plan_bytes(None, 1, ctypes.byref(b)) == f3c.F3C_EINVAL
+    assert L.f3c_state_plan_times(None, None, 0, None, 0, None) == f3c.F3C_EINVAL
+
+
 def test_guidance_interval_matches_oracle():
     from oracle import schedule as osched
     for eta in (1.0, 2.0, 3.0):

@@ -15,7 +15,7 @@ import numpy as np
 import pytest
 
 from helpers import Pair, depth_variant, max_rel, oracle_selection, rel_l2, say, to_dev
-from oracle import sampler, schedule
+from oracle import dit, sampler, schedule
 from paper_2511_22533_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -264,6 +264,117 @@ def test_graph_capture_of_a_trajectory_replays_exactly(torch):
     trajectory(x2)
     torch.cuda.synchronize()
     assert torch.equal(x2, eager)
+
+
+_PLAN_CFGS = [synth.TINY, synth.ModelConfig(grid=4, width=1024, depth=3, heads=16, cond_tokens=8, cond_width=64,
+                                            dtype="bf16")]
+
+
+@pytest.mark.parametrize("cfg", _PLAN_CFGS, ids=["tiny_f32", "w1024_bf16"])
+def test_modulation_plan_equals_per_step_modulation_bitwise(torch, cfg):
+    """The planned modulation of 11 times (one pass of 8 times, one of 3)
+    equals the per-time modulation entry bit for bit, and the oracle's
+    modulation within the per-step tolerance."""
+    from paper_2511_22533_amd import f3c
+    W = synth.make_weights(cfg, seed=2, scale=0.05)
+    m = f3c.Model(cfg).load(W)
+    st = f3c.State(m, 1)
+    times = [float(t) for t in schedule.time_grid(10, 3.0)[:-1]] + [0.5, 0.0]
+    say("plan", cfg.dtype, len(times), "times")
+    st.plan_times(times)
+    torch.cuda.synchronize()
+    R = cfg.depth * 6 * cfg.width
+    plan = st.plan_buf[: len(times) * R * 4].view(torch.float32).reshape(len(times), R).cpu().numpy()
+    om = dit.Model(cfg, W)
+    tol = 1e-4 if cfg.dtype == "f32" else 5e-3
+    for i, t in enumerate(times):
+        want = m.modulation(t).cpu().numpy().ravel()
+        assert np.array_equal(plan[i].view(np.uint32), want.view(np.uint32)), f"time {i} ({t})"
+    assert max_rel(plan[3], om.modulation(times[3]).ravel()) < tol
+
+
+def test_planned_trajectory_is_bit_identical(torch):
+    """A trajectory whose step times are planned (all of them, some of them,
+    then the plan cleared) gives the unplanned trajectory bit for bit; a step
+    at a planned time launches no modulation kernels."""
+    from paper_2511_22533_amd import f3c
+    cfg = depth_variant(synth.TRELLIS16, 2)
+    model = f3c.Model(cfg).load(synth.make_weights(cfg, seed=0))
+    state = f3c.State(model, 1)
+    cond = to_dev(synth.make_cond(cfg, 1))
+    x_T = to_dev(synth.make_noise(cfg, 1))
+    times = [float(t) for t in schedule.time_grid(6, 3.0)]
+    quotas = [[0], [0], [1024], [2048], [3000], [3276]]
+
+    def trajectory():
+        x = x_T.clone()
+        state.reset()
+        state.set_cond(cond)
+        state.profile(["mod"])
+        state.profile_reset()
+        for k, q in enumerate(quotas):
+            if any(q):
+                state.cached_step(x, times[k], times[k + 1], q)
+            else:
+                state.full_step(x, times[k], times[k + 1])
+        torch.cuda.synchronize()
+        n_mod = state.profile_read()["mod"]["launches"]
+        state.profile(False)
+        return x, n_mod
+
+    say("unplanned trajectory")
+    ref, n = trajectory()
+    assert n == 6
+    for plan, mod_calls in ((times[:-1], 0), (times[1:4:2], 4), ([], 6)):
+        say("planned", len(plan), "times")
+        state.plan_times(plan)
+        x, n = trajectory()
+        assert n == mod_calls
+        assert torch.equal(x, ref), f"plan of {len(plan)} times"
+
+
+def test_modulation_plan_validation(torch):
+    """Bad plans are refused before anything is enqueued and keep the previous
+    plan; the binding reuses its buffer."""
+    import ctypes
+    from paper_2511_22533_amd import f3c
+    cfg = synth.TINY
+    m = f3c.Model(cfg).load(synth.make_weights(cfg, seed=0))
+    st = f3c.State(m, 1)
+    st.set_cond(to_dev(synth.make_cond(cfg, 1)))
+    st.plan_times([0.9, 0.8])
+    buf = st.plan_buf
+    L = f3c.lib()
+    need = ctypes.c_size_t()
+    assert L.f3c_plan_bytes(m.h, 2, ctypes.byref(need)) == f3c.F3C_OK
+    R = cfg.depth * 6 * cfg.width
+
+    def a256(v):
+        return (v + 255) // 256 * 256
+    assert need.value == a256(2 * R * 4) + a256(2 * 2 * cfg.width * 4)
+    assert L.f3c_plan_bytes(m.h, -1, ctypes.byref(need)) == f3c.F3C_EINVAL
+    assert L.f3c_plan_bytes(m.h, 1025, ctypes.byref(need)) == f3c.F3C_EINVAL
+    ptr, nb = buf.data_ptr(), buf.numel()
+    t2 = (ctypes.c_double * 2)(0.7, float("nan"))
+    ok = (ctypes.c_double * 2)(0.7, 0.6)
+    assert L.f3c_state_plan_times(st.h, t2, 2, ptr, nb, None) == f3c.F3C_EINVAL
+    assert b"not finite" in L.f3c_last_error()
+    assert L.f3c_state_plan_times(st.h, ok, 2, ptr + 16, nb - 16, None) == f3c.F3C_EINVAL
+    assert L.f3c_state_plan_times(st.h, ok, 2, ptr, 1024, None) == f3c.F3C_ENOMEM
+    assert L.f3c_state_plan_times(st.h, None, 2, ptr, nb, None) == f3c.F3C_EINVAL
+    assert L.f3c_state_plan_times(st.h, ok, 2000, ptr, nb, None) == f3c.F3C_EINVAL
+    # the plan of 0.9 and 0.8 is still in place
+    x = to_dev(synth.make_noise(cfg, 1))
+    st.profile(["mod"])
+    st.profile_reset()
+    st.full_step(x, 0.9, 0.8)
+    st.full_step(x, 0.8, 0.75)
+    st.full_step(x, 0.75, 0.7)
+    torch.cuda.synchronize()
+    assert st.profile_read()["mod"]["launches"] == 1
+    st.profile(False)
+    st.plan_times([0.5])
+    assert st.plan_buf is buf
 
 
 def test_trellis16_cached_step_full_depth(torch):
