@@ -339,26 +339,36 @@ __global__ __launch_bounds__(256) void k_gemv_tn(const T* __restrict__ Wt, const
 #pragma unroll
     for (int e = 0; e < V; ++e) acc[i][e] = 0.0f;
   if (r0 < R) {
+    // Sixteen weight loads in flight per wave, issued before any of them is
+    // used (one wave per SIMD at this grid; left to itself the compiler waits
+    // on each load right after issuing it). The order of the sums is unchanged.
+    constexpr int U = 16;                           // K/4 is a multiple of 32
     const T* w = Wt + (size_t)k0 * R + r0;
-#pragma unroll 4
-    for (int k = 0; k < kq; ++k) {
-      float wf[V];
-      if constexpr (sizeof(T) == 2) {
-        const bf16x8 wv = *reinterpret_cast<const bf16x8*>(w + (size_t)k * R);
+    for (int kb = 0; kb < kq; kb += U) {
+      u32x4 raw[U];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) wf[e] = (float)wv[e];
-      } else {
-        const float4 wv = *reinterpret_cast<const float4*>(w + (size_t)k * R);
-        wf[0] = wv.x;
-        wf[1] = wv.y;
-        wf[2] = wv.z;
-        wf[3] = wv.w;
-      }
+      for (int u = 0; u < U; ++u) raw[u] = *reinterpret_cast<const u32x4*>(w + (size_t)(kb + u) * R);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int i = 0; i < NT; ++i) {
-        const float xv = xs[i * K + k0 + k];
+      for (int u = 0; u < U; ++u) {
+        float wf[V];
+        if constexpr (sizeof(T) == 2) {
+          const bf16x8 wv = __builtin_bit_cast(bf16x8, raw[u]);
 #pragma unroll
-        for (int e = 0; e < V; ++e) acc[i][e] += wf[e] * xv;
+          for (int e = 0; e < 8; ++e) wf[e] = (float)wv[e];
+        } else {
+          const float4 wv = __builtin_bit_cast(float4, raw[u]);
+          wf[0] = wv.x;
+          wf[1] = wv.y;
+          wf[2] = wv.z;
+          wf[3] = wv.w;
+        }
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+          const float xv = xs[i * K + k0 + kb + u];
+#pragma unroll
+          for (int e = 0; e < V; ++e) acc[i][e] += wf[e] * xv;
+        }
       }
     }
   }
@@ -481,7 +491,7 @@ hipError_t launch_gemv_t(int dt, const void* Wt, const float* bias, const float*
 
 hipError_t launch_gemv_tn(int dt, const void* Wt, const float* bias, const float* x, int ldx, int nt, int R, int K,
                           float* y, int ldy, hipStream_t s) {
-  if (nt < 1 || nt > kGemvChunk || K % 4) return hipErrorInvalidValue;
+  if (nt < 1 || nt > kGemvChunk || K % 32) return hipErrorInvalidValue;
   const int per_block = 64 * (dt == DT_BF16 ? 8 : 4);
   dim3 grid((R + per_block - 1) / per_block);
   const size_t lds = (size_t)kGemvChunk * K * sizeof(float);
