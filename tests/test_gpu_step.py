@@ -218,8 +218,8 @@ def test_two_states_on_two_streams_match_sequential(torch):
 
 
 def test_graph_capture_of_a_trajectory_replays_exactly(torch):
-    """A whole trajectory (state reset, condition K/V, cached steps) captured
-    in one HIP graph: the library records only kernels on the caller's stream
+    """A whole trajectory (state reset, condition K/V, modulation plan, cached
+    steps) captured in one HIP graph: the library records only kernels on the caller's stream
     (the reset zeroes the caches with a kernel, not a memset node), so every
     replay, with eager work and synchronisations in between, gives the eager
     trajectory bit for bit."""
@@ -235,6 +235,7 @@ def test_graph_capture_of_a_trajectory_replays_exactly(torch):
     def trajectory(x):
         state.reset()
         state.set_cond(cond)
+        state.plan_times(times[:-1])
         for k, q in enumerate(quotas):
             state.cached_step(x, times[k], times[k + 1], q)
 
@@ -331,6 +332,36 @@ def test_planned_trajectory_is_bit_identical(torch):
         x, n = trajectory()
         assert n == mod_calls
         assert torch.equal(x, ref), f"plan of {len(plan)} times"
+
+
+def test_planned_guided_trajectory_is_bit_identical(torch):
+    """Guided steps read the planned modulation for both passes: a guided
+    trajectory with its times planned equals the unplanned one bit for bit."""
+    from paper_2511_22533_amd import f3c
+    cfg = depth_variant(synth.TRELLIS16, 2)
+    model = f3c.Model(cfg).load(synth.make_weights(cfg, seed=0))
+    state = f3c.State(model, 2, guided=True)
+    cond = to_dev(synth.make_cond(cfg, 2))
+    uncond = to_dev(synth.make_uncond(cfg, 2))
+    x_T = to_dev(synth.make_noise(cfg, 2))
+    times = [float(t) for t in schedule.time_grid(4, 3.0)]
+    quotas = [None, [1000, 3000], [2048, 0], [3276, 3276]]
+
+    def trajectory():
+        x = x_T.clone()
+        state.reset()
+        state.set_cond(cond)
+        state.set_uncond(uncond)
+        for k, q in enumerate(quotas):
+            state.guided_step(x, times[k], times[k + 1], q, 3.0)
+        torch.cuda.synchronize()
+        return x
+
+    say("guided, unplanned")
+    ref = trajectory()
+    state.plan_times(times[:-1])
+    say("guided, planned")
+    assert torch.equal(trajectory(), ref)
 
 
 def test_modulation_plan_validation(torch):
