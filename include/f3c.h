@@ -153,8 +153,9 @@ int f3c_set_cond(f3c_state* s, const float* cond_dev, f3c_stream stream);
 int f3c_set_uncond(f3c_state* s, const float* uncond_dev, f3c_stream stream);
 
 /* Modulation plan. The timestep modulation of every block (the time embedding
- * followed by the 6*width adaLN vector of each block) depends only on t and
- * the weights. f3c_state_plan_times computes it for the n times t_host[0..n-1]
+ * followed by the 6*width adaLN vector of each block; the "Modulation" term of
+ * the supplement's FLOPs list, counted per sample and step) depends only on t
+ * and the weights. f3c_state_plan_times computes it for the n times t_host[0..n-1]
  * (normally the trajectory's time grid) in ceil(n / 8) passes over the
  * modulation weights, instead of one pass per step, into the caller's device
  * buffer plan_dev (256-byte aligned, at least f3c_plan_bytes(m, n) bytes):
