@@ -6,6 +6,7 @@
 //   f3c_drive [--grid G] [--width D] [--depth L] [--heads H] [--cond NC]
 //             [--cond-width DC] [--f32] [--batch B] [--steps T] [--eta E]
 //             [--quotas c1,c2,...] [--repeat R] [--copy-mib M] [--graph]
+//   f3c_drive --peaks
 //
 // Defaults: the 24-block, width-1024 bf16 model on a 16^3 grid with 1374 x
 // 1024 condition tokens, 25 steps with the eta = 3 time shift (Eq. S1), every
@@ -21,8 +22,13 @@
 // known-size reference for hardware byte counters.
 //
 // --graph captures the T steps of a trajectory once into a HIP graph and
-// replays it; the per-trajectory cache reset (a memset), the copy of x_T and
-// the condition K/V stay eager launches before each replay.
+// replays it; the per-trajectory cache reset, the copy of x_T, the condition
+// K/V and the modulation plan stay eager launches before each replay.
+//
+// --peaks measures what the chip sustains, for the rooflines, and exits: the
+// dense bf16 matrix-core rate (every wave issues independent
+// v_mfma_f32_32x32x16_bf16 on register operands, four waves per SIMD) and the
+// HBM bandwidth of a plain 1 GiB float4 copy (bytes read plus written).
 #include <hip/hip_runtime.h>
 
 #include <chrono>
@@ -40,6 +46,28 @@ namespace {
 __global__ void k_copy_ref(const float4* __restrict__ src, float4* __restrict__ dst, size_t n) {
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
     dst[i] = src[i];
+}
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+__global__ __launch_bounds__(256) void k_mfma_peak(float* __restrict__ out, int iters, float seed) {
+  bf16x8_t a, b;
+  for (int e = 0; e < 8; ++e) {
+    a[e] = (__bf16)(seed * (float)(threadIdx.x + e));
+    b[e] = (__bf16)(seed - (float)e);
+  }
+  f32x16_t acc[8];
+  for (int i = 0; i < 8; ++i)
+    for (int e = 0; e < 16; ++e) acc[i][e] = 0.0f;
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[i], 0, 0, 0);
+  }
+  float sum = 0.0f;
+  for (int i = 0; i < 8; ++i)
+    for (int e = 0; e < 16; ++e) sum += acc[i][e];
+  out[(size_t)blockIdx.x * blockDim.x + threadIdx.x] = sum;
 }
 
 [[noreturn]] void die(const char* what) {
@@ -107,7 +135,7 @@ int main(int argc, char** argv) {
   cfg.cond_width = 1024;
   cfg.dtype = F3C_BF16;
   int batch = 1, steps = 25, repeat = 1, copy_mib = 0;
-  bool use_graph = false;
+  bool use_graph = false, peaks = false;
   double eta = 3.0;
   std::vector<int> quotas;
   for (int i = 1; i < argc; ++i) {
@@ -130,6 +158,7 @@ int main(int argc, char** argv) {
     else if (a == "--repeat") repeat = std::atoi(val());
     else if (a == "--copy-mib") copy_mib = std::atoi(val());
     else if (a == "--graph") use_graph = true;
+    else if (a == "--peaks") peaks = true;
     else die(("unknown argument " + a).c_str());
   }
   if (quotas.empty()) quotas.assign(steps, 0);
@@ -142,6 +171,56 @@ int main(int argc, char** argv) {
   hip_check(hipSetDevice(0), "hipSetDevice");
   hipStream_t st;
   hip_check(hipStreamCreate(&st), "hipStreamCreate");
+
+  if (peaks) {
+    hipEvent_t p0, p1;
+    hip_check(hipEventCreate(&p0), "hipEventCreate");
+    hip_check(hipEventCreate(&p1), "hipEventCreate");
+    int cus = 0;
+    hip_check(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, 0), "hipDeviceGetAttribute");
+    // Matrix cores: four 4-wave workgroups per CU, 4096 x 8 MFMAs per wave.
+    const int blocks = 4 * cus, iters = 4096;
+    float* out = nullptr;
+    hip_check(hipMalloc(&out, (size_t)blocks * 256 * sizeof(float)), "hipMalloc");
+    hipLaunchKernelGGL(k_mfma_peak, dim3(blocks), dim3(256), 0, st, out, 16, 1.0f);
+    hip_check(hipGetLastError(), "k_mfma_peak");
+    float best = 1e30f;
+    for (int r = 0; r < 3; ++r) {
+      hip_check(hipEventRecord(p0, st), "hipEventRecord");
+      hipLaunchKernelGGL(k_mfma_peak, dim3(blocks), dim3(256), 0, st, out, iters, 1.0f);
+      hip_check(hipEventRecord(p1, st), "hipEventRecord");
+      hip_check(hipEventSynchronize(p1), "k_mfma_peak");
+      float ms = 0.0f;
+      hip_check(hipEventElapsedTime(&ms, p0, p1), "hipEventElapsedTime");
+      best = std::fmin(best, ms);
+    }
+    const double flops = (double)blocks * 4 * iters * 8 * 32768.0;
+    std::printf("peak: bf16 matrix cores %.1f TFLOP/s on %d CUs (%.1f%% of 2500)\n", flops / best * 1e-9, cus,
+                flops / best * 1e-9 / 25.0);
+    hip_check(hipFree(out), "hipFree");
+    // HBM: a 1 GiB float4 copy, best of 10 (bytes read plus written).
+    const size_t n4 = ((size_t)1 << 30) / sizeof(float4);
+    float4 *src, *dst;
+    hip_check(hipMalloc(&src, n4 * sizeof(float4)), "hipMalloc");
+    hip_check(hipMalloc(&dst, n4 * sizeof(float4)), "hipMalloc");
+    hip_check(hipMemsetAsync(src, 0, n4 * sizeof(float4), st), "hipMemsetAsync");
+    hipLaunchKernelGGL(k_copy_ref, dim3(4096), dim3(256), 0, st, src, dst, n4);
+    best = 1e30f;
+    for (int r = 0; r < 10; ++r) {
+      hip_check(hipEventRecord(p0, st), "hipEventRecord");
+      hipLaunchKernelGGL(k_copy_ref, dim3(4096), dim3(256), 0, st, src, dst, n4);
+      hip_check(hipEventRecord(p1, st), "hipEventRecord");
+      hip_check(hipEventSynchronize(p1), "k_copy_ref");
+      float ms = 0.0f;
+      hip_check(hipEventElapsedTime(&ms, p0, p1), "hipEventElapsedTime");
+      best = std::fmin(best, ms);
+    }
+    const double bytes = 2.0 * n4 * sizeof(float4);
+    std::printf("peak: HBM copy %.0f GB/s (%.1f%% of 8000)\n", bytes / best * 1e-6, bytes / best * 1e-6 / 80.0);
+    hip_check(hipFree(src), "hipFree");
+    hip_check(hipFree(dst), "hipFree");
+    return 0;
+  }
 
   if (copy_mib > 0) {
     const size_t n4 = ((size_t)copy_mib << 20) / sizeof(float4);
