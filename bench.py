@@ -225,6 +225,18 @@ def hbm_sweep():
     print(json.dumps({"mode": "hbm_sweep", "peak_GB/s": PEAK_HBM_GBS, "rows": rows_out}), flush=True)
 
 
+def _cpu_model() -> str:
+    """The host CPU's model name from /proc/cpuinfo (empty if unavailable)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return ""
+
+
 def cpu_baseline(w, W, cond, x_T, quotas, times, depth, guided=None):
     """Time the CPU oracle on a bounded sample: one full step and one cached step
     (the schedule's last quota), at `depth` blocks, scaled to the whole model and
@@ -269,6 +281,7 @@ def cpu_baseline(w, W, cond, x_T, quotas, times, depth, guided=None):
         "value": steps / total,
         "unit": "steps/s",
         "cores": threads,
+        "cpu_model": _cpu_model(),
         "kind": "oracle",
         "sample": (f"float64 NumPy oracle, {depth} of {cfg.depth} blocks: one full step ({N} tokens, "
                    f"{t_full:.2f} s) and one cached step ({N - n_last} active, {t_cached:.2f} s), scaled by "
