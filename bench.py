@@ -1,19 +1,22 @@
 """Throughput of the cached sparse-structure flow-DiT sampler on one MI355X.
 
-Workload (default): the 24-block, width-1024 TRELLIS-shaped sparse-structure
-transformer on a 16^3 latent grid (4096 tokens, 8 channels), 16 heads of 64,
-cross-attention to 1374 condition tokens of width 1024, bf16, batch 1, 25
-shifted Euler steps: 5 full steps, then a seeded logistic cache quota that
-reaches 80% cached tokens at step 25. Weights, noise and condition tokens are
-seeded synthetic data (no trained weights or image features exist here).
+Workload (default, ``trellis32_cached``): the 12-block, width-1024
+TRELLIS-shaped sparse-structure transformer on a 32^3 latent grid (32768
+tokens, 8 channels), 16 heads of 64, cross-attention to 1374 condition tokens
+of width 1024, bf16, batch 1, 25 shifted Euler steps: 5 full steps, then a
+fixed 70% cache quota (9831 active tokens per cached step). Weights, noise and
+condition tokens are seeded synthetic data (no trained weights or image
+features exist here). The 24-block 16^3 workload with the logistic quota
+(``trellis16_cached``) is measured after it over one whole trajectory and
+reported in the ``secondary`` field.
 
 A "step" is one denoising step of that schedule: stability scoring and top-k
-selection, gather + embedding, timestep modulation, 24 blocks on the active
+selection, gather + embedding, timestep modulation, the blocks on the active
 tokens, output projection and the merge/Euler/cache update. K timed steps walk
-through the schedule and wrap around; every trajectory start re-zeroes the
-caches, reloads x_T, recomputes the condition keys/values and plans the
-timestep modulation of all the trajectory's step times (one pass over the
-modulation weights per 8 times) inside the timed region.
+through the schedule from a trajectory start and wrap around; every trajectory
+start re-zeroes the caches, reloads x_T, recomputes the condition keys/values
+and plans the timestep modulation of all the trajectory's step times (one pass
+over the modulation weights per 8 times) inside the timed region.
 
 Prints one JSON line. ``value`` is denoising steps per second; the line also
 carries active tokens/s, the whole-step MFMA fraction (FLOPs model of the
@@ -50,9 +53,12 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=25)
-    ap.add_argument("--workload", default="trellis16_cached")
+    ap.add_argument("--workload", default="trellis32_cached")
+    ap.add_argument("--secondary", default="trellis16_cached",
+                    help="workload timed over one whole trajectory after the main one ('' = none)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--cpu-depth", type=int, default=8, help="oracle blocks timed (0 = full depth)")
+    ap.add_argument("--cpu-depth", type=int, default=None,
+                    help="oracle blocks timed (default: as many as keep the sample near 15 s; 0 = full depth)")
     ap.add_argument("--copy-ref-mb", type=int, default=0,
                     help="first run one plain device-to-device copy of this many MiB (a known-size reference "
                          "for hardware byte counters)")
@@ -66,34 +72,46 @@ def parse():
     return ap.parse_args()
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "trellis16_cached_traffic.md")
-TRAFFIC_WORKLOAD = "trellis16_cached"
+def counter_traffic(cls: str, workload: str, timed_ks):
+    """HBM-side bytes per launch of a kernel class over the timed launches, from
+    the committed FETCH_SIZE / WRITE_SIZE counter summary of the workload's
+    trajectory (profiles/<workload>_traffic.md), or (None, reason).
 
-
-def counter_traffic(cls: str, workload: str):
-    """HBM-side bytes per call of a kernel class from the committed FETCH_SIZE /
-    WRITE_SIZE counter summary of the trellis16_cached trajectory, or (None,
-    reason). The figure is used only while the SHA-256 of the kernel's source
-    files equals the one recorded with the counters."""
+    The summary holds one line per step k of the trajectory and class:
+    "traffic <cls> k=<k>: <bytes> bytes over <calls> calls; sources <files>
+    sha256 <hex>". The figure is the byte total of the timed steps' launches
+    over their count (the same launches as the roofline's achieved rate), and
+    is used only while the SHA-256 of the kernel's source files equals the one
+    recorded with the counters."""
     import hashlib
     import re
-    if workload != TRAFFIC_WORKLOAD:
-        return None, f"counters were taken on {TRAFFIC_WORKLOAD} only"
-    if not os.path.exists(TRAFFIC_FILE):
-        return None, "no counter summary"
-    pat = re.compile(r"traffic (\w+): (\d+) bytes per call; sources (\S+) sha256 ([0-9a-f]{64})")
-    for line in open(TRAFFIC_FILE):
+    path = os.path.join(ROOT, "profiles", f"{workload}_traffic.md")
+    if not os.path.exists(path):
+        return None, f"no counter summary for {workload}"
+    pat = re.compile(r"traffic (\w+) k=(\d+): (\d+) bytes over (\d+) calls; sources (\S+) sha256 ([0-9a-f]{64})")
+    per_k = {}
+    sources = None
+    for line in open(path):
         m = pat.search(line)
         if not m or m.group(1) != cls:
             continue
-        h = hashlib.sha256()
-        for name in m.group(3).split("+"):
-            with open(os.path.join(ROOT, "paper_2511_22533_amd", "csrc", name), "rb") as fh:
-                h.update(fh.read())
-        if h.hexdigest() != m.group(4):
-            return None, "kernel sources changed since the counters were taken"
-        return int(m.group(2)), "rocprofv3 FETCH_SIZE + WRITE_SIZE, scaled by a 256 MiB copy reference"
-    return None, f"no counter line for {cls}"
+        per_k[int(m.group(2))] = (int(m.group(3)), int(m.group(4)))
+        sources = (m.group(5), m.group(6))
+    if not per_k:
+        return None, f"no counter line for {cls}"
+    h = hashlib.sha256()
+    for name in sources[0].split("+"):
+        with open(os.path.join(ROOT, "paper_2511_22533_amd", "csrc", name), "rb") as fh:
+            h.update(fh.read())
+    if h.hexdigest() != sources[1]:
+        return None, "kernel sources changed since the counters were taken"
+    if any(k not in per_k for k in timed_ks):
+        return None, "counter summary does not cover every timed step"
+    total = sum(per_k[k][0] for k in timed_ks)
+    calls = sum(per_k[k][1] for k in timed_ks)
+    return (round(total / calls) if calls else None,
+            "rocprofv3 FETCH_SIZE + WRITE_SIZE per dispatch, scaled by a 256 MiB copy reference, over the timed "
+            "steps' launches")
 
 
 def _event_time_ms(torch, fn, reps):
@@ -237,14 +255,25 @@ def _cpu_model() -> str:
     return ""
 
 
-def cpu_baseline(w, W, cond, x_T, quotas, times, depth, guided=None):
-    """Time the CPU oracle on a bounded sample: one full step and one cached step
-    (the schedule's last quota), at `depth` blocks, scaled to the whole model and
-    interpolated over the schedule by the FLOPs model. A guided step counts as
-    two transformer passes (the oracle runs them one after the other)."""
-    from oracle import dit, flops, sampler, ssc
+CPU_SAMPLE_S = 15.0   # target seconds of oracle work in the CPU baseline sample
+
+
+def cpu_baseline(w, W, cond, x_T, quotas, times, depth=None, guided=None):
+    """Time the CPU oracle on a bounded sample of the workload and scale it to
+    steps/s over the schedule.
+
+    The sample is one cached step at the schedule's largest quota, at `depth`
+    blocks (default: one block for the 12-block 32^3 model, eight for the
+    24-block 16^3 model), then one full step at the same depth if the FLOPs
+    model predicts it fits the CPU_SAMPLE_S budget from the cached step's rate;
+    otherwise the full step's time is that prediction (labelled as such). Step
+    times are scaled by the block count and interpolated over the schedule's
+    active counts with the FLOPs model. A guided step counts as two passes."""
+    from oracle import dit, flops, sampler
     from paper_2511_22533_amd import synth
     cfg = w.model
+    if depth is None:
+        depth = 1 if cfg.tokens > 4096 else min(8, cfg.depth)
     depth = depth or cfg.depth
     sub = synth.ModelConfig(grid=cfg.grid, width=cfg.width, depth=depth, heads=cfg.heads,
                             cond_tokens=cfg.cond_tokens, cond_width=cfg.cond_width, dtype=cfg.dtype,
@@ -255,26 +284,33 @@ def cpu_baseline(w, W, cond, x_T, quotas, times, depth, guided=None):
     rng = np.random.default_rng(0)
     st.v_cache[:] = rng.standard_normal(st.v_cache.shape).astype(np.float32)
     st.v_prev[:] = rng.standard_normal(st.v_prev.shape).astype(np.float32)
-    n_last = int(quotas[-1][0])
-    t0 = time.perf_counter()
-    sampler.step(st, vel, times[0], times[1], [0] * w.batch)
-    t_full = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    sampler.step(st, vel, times[-2], times[-1], quotas[-1])
-    t_cached = time.perf_counter() - t0
-    scale = cfg.depth / depth
+    k_max = int(np.argmax(quotas.sum(axis=1)))
+    q_max = [int(c) for c in quotas[k_max]]
     N = cfg.tokens
-    f_full = flops.forward_flops(cfg, N, 1)
-    f_last = flops.forward_flops(cfg, N - n_last, 1)
+    t0 = time.perf_counter()
+    sampler.step(st, vel, times[k_max], times[k_max + 1], q_max)
+    t_cached = time.perf_counter() - t0
+    f_full = sum(flops.forward_flops(sub, N, 1) for _ in range(w.batch))
+    f_cached = sum(flops.forward_flops(sub, N - c, 1) for c in q_max)
+    predicted_full = t_cached * f_full / f_cached if f_cached > 0 else t_cached
+    if predicted_full <= CPU_SAMPLE_S:
+        t0 = time.perf_counter()
+        sampler.step(st, vel, times[0], times[1], [0] * w.batch)
+        t_full = time.perf_counter() - t0
+        full_how = f"one full step ({N} tokens per sample, {t_full:.2f} s)"
+    else:
+        t_full = predicted_full
+        full_how = (f"the full step ({N} tokens per sample) not run: its time, {t_full:.1f} s, is the cached "
+                    f"step's rate times the FLOPs model's full/cached ratio")
+    scale = cfg.depth / depth
     total = 0.0
     tokens = 0
     for k, q in enumerate(quotas):
-        n = N - int(q[0])
-        f = flops.forward_flops(cfg, n, 1)
-        frac = (f - f_last) / (f_full - f_last) if f_full > f_last else 1.0
+        f = sum(flops.forward_flops(sub, N - int(c), 1) for c in q)
+        frac = (f - f_cached) / (f_full - f_cached) if f_full > f_cached else 1.0
         passes = 2 if guided is not None and guided[k] else 1
         total += passes * scale * (t_cached + (t_full - t_cached) * frac)
-        tokens += n * w.batch
+        tokens += sum(N - int(c) for c in q)
     steps = len(quotas)
     threads = len(os.sched_getaffinity(0))
     return {
@@ -283,13 +319,75 @@ def cpu_baseline(w, W, cond, x_T, quotas, times, depth, guided=None):
         "cores": threads,
         "cpu_model": _cpu_model(),
         "kind": "oracle",
-        "sample": (f"float64 NumPy oracle, {depth} of {cfg.depth} blocks: one full step ({N} tokens, "
-                   f"{t_full:.2f} s) and one cached step ({N - n_last} active, {t_cached:.2f} s), scaled by "
-                   f"{scale:g} to all blocks and interpolated over the {steps}-step schedule with the FLOPs model"
+        "sample": (f"float64 NumPy oracle, {depth} of {cfg.depth} blocks: one cached step at the schedule's "
+                   f"largest quota ({sum(N - c for c in q_max)} active tokens, {t_cached:.2f} s) and {full_how}; "
+                   f"scaled by {scale:g} to all blocks and interpolated over the {steps}-step schedule with the "
+                   f"FLOPs model"
                    + (f", guided steps counted as two passes ({sum(guided)} of {steps})" if guided is not None else "")),
         "active_tokens_per_s": tokens / total,
-        "seconds_measured": t_full + t_cached,
+        "seconds_measured": t_cached + (t_full if predicted_full <= CPU_SAMPLE_S else 0.0),
     }
+
+
+class Runner:
+    """One workload on the library: model, state, seeded inputs and the step loop."""
+
+    def __init__(self, name: str):
+        import torch
+        from paper_2511_22533_amd import f3c, synth
+        self.torch, self.f3c = torch, f3c
+        w = self.w = synth.WORKLOADS[name]
+        cfg = self.cfg = w.model
+        self.W = synth.make_weights(cfg)
+        self.cond = synth.make_cond(cfg, w.batch)
+        self.x_T = synth.make_noise(cfg, w.batch)
+        self.quotas = synth.quota_schedule(w)
+        self.times = f3c.time_grid(w.steps, w.shift)
+        self.model = f3c.Model(cfg).load(self.W)
+        self.guided = [w.guidance > 0 and f3c.guidance_active(float(t), *w.guidance_interval)
+                       for t in self.times[:-1]]
+        self.state = f3c.State(self.model, w.batch, guided=any(self.guided))
+        self.x = torch.empty((w.batch, cfg.tokens, cfg.in_ch), dtype=torch.float32, device="cuda")
+        self.x_T_dev = torch.from_numpy(self.x_T).cuda()
+        self.cond_dev = torch.from_numpy(self.cond).cuda()
+        self.uncond_dev = (torch.from_numpy(synth.make_uncond(cfg, w.batch)).cuda() if any(self.guided)
+                           else None)
+        self.T = w.steps
+
+    def step(self, i: int) -> int:
+        """Step i of the endless schedule (a trajectory start every T steps); returns its active tokens."""
+        w, cfg, st, x, times = self.w, self.cfg, self.state, self.x, self.times
+        k = i % self.T
+        if k == 0:
+            st.reset()
+            x.copy_(self.x_T_dev)
+            st.set_cond(self.cond_dev)
+            if self.uncond_dev is not None:
+                st.set_uncond(self.uncond_dev)
+            st.plan_times(times[:-1])
+        q = self.quotas[k].tolist()
+        if self.guided[k]:
+            st.guided_step(x, float(times[k]), float(times[k + 1]), q if any(q) else None, w.guidance)
+        elif any(q):
+            st.cached_step(x, float(times[k]), float(times[k + 1]), q)
+        else:
+            st.full_step(x, float(times[k]), float(times[k + 1]))
+        return sum(cfg.tokens - c for c in q)
+
+    def step_flops(self, i: int) -> float:
+        k = i % self.T
+        return (2 if self.guided[k] else 1) * sum(self.f3c.forward_flops(self.cfg, self.cfg.tokens - int(c), 1)
+                                                  for c in self.quotas[k])
+
+    def trajectory_ms(self, reps: int = 1) -> float:
+        """Wall time of whole trajectories (host clock around synchronised runs), ms per trajectory."""
+        torch = self.torch
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(reps * self.T):
+            self.step(i)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3 / reps
 
 
 def main():
@@ -304,13 +402,10 @@ def main():
         return
 
     import torch
-    from paper_2511_22533_amd import f3c, synth
+    from paper_2511_22533_amd import f3c
     from paper_2511_22533_amd.f3c import PROF_CLASSES
 
-    w = synth.WORKLOADS[args.workload]
-    cfg = w.model
     torch.cuda.set_device(0)
-    print(f"[bench] workload {w.name}: {w.description}", file=sys.stderr, flush=True)
     if args.copy_ref_mb:
         src = torch.ones(args.copy_ref_mb << 18, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
@@ -319,41 +414,14 @@ def main():
         torch.cuda.synchronize()
         print(f"[bench] reference copy of {args.copy_ref_mb} MiB done", file=sys.stderr, flush=True)
         del src, dst
-    W = synth.make_weights(cfg)
-    cond = synth.make_cond(cfg, w.batch)
-    x_T = synth.make_noise(cfg, w.batch)
-    quotas = synth.quota_schedule(w)
-    times = f3c.time_grid(w.steps, w.shift)
-    model = f3c.Model(cfg).load(W)
-    guided = [w.guidance > 0 and f3c.guidance_active(float(t), *w.guidance_interval) for t in times[:-1]]
-    state = f3c.State(model, w.batch, guided=any(guided))
-    x = torch.empty((w.batch, cfg.tokens, cfg.in_ch), dtype=torch.float32, device="cuda")
-    x_T_dev = torch.from_numpy(x_T).cuda()
-    cond_dev = torch.from_numpy(cond).cuda()
-    uncond_dev = torch.from_numpy(synth.make_uncond(cfg, w.batch)).cuda() if any(guided) else None
-    T = w.steps
-
-    def run_step(i):
-        k = i % T
-        if k == 0:
-            state.reset()
-            x.copy_(x_T_dev)
-            state.set_cond(cond_dev)
-            if uncond_dev is not None:
-                state.set_uncond(uncond_dev)
-            state.plan_times(times[:-1])
-        q = quotas[k].tolist()
-        if guided[k]:
-            state.guided_step(x, float(times[k]), float(times[k + 1]), q if any(q) else None, w.guidance)
-        elif any(q):
-            state.cached_step(x, float(times[k]), float(times[k + 1]), q)
-        else:
-            state.full_step(x, float(times[k]), float(times[k + 1]))
-        return sum(cfg.tokens - c for c in q)
+    run = Runner(args.workload)
+    w, cfg, state, x, times, quotas, guided, T = (run.w, run.cfg, run.state, run.x, run.times, run.quotas,
+                                                  run.guided, run.T)
+    print(f"[bench] workload {w.name}: {w.description}", file=sys.stderr, flush=True)
 
     # warmup (untimed)
     for i in range(args.warmup):
-        run_step(i)
+        run.step(i)
     torch.cuda.synchronize()
     print(f"[bench] warmup {args.warmup} steps done", file=sys.stderr, flush=True)
 
@@ -361,7 +429,7 @@ def main():
     state.profile(True)
     state.profile_reset()
     for i in range(T):
-        run_step(i)
+        run.step(i)
     torch.cuda.synchronize()
     calib = state.profile_read()
     state.profile(False)
@@ -378,22 +446,23 @@ def main():
     active = 0
     flop_total = 0.0
     for i in range(args.steps):
-        n_act = run_step(i)
-        active += n_act
-        flop_total += (2 if guided[i % T] else 1) * sum(f3c.forward_flops(cfg, cfg.tokens - int(c), 1)
-                                                         for c in quotas[i % T])
+        active += run.step(i)
+        flop_total += run.step_flops(i)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     prof = state.profile_read()[dominant]
     state.profile(False)
     print(f"[bench] timed {args.steps} steps in {elapsed * 1e3:.1f} ms", file=sys.stderr, flush=True)
 
+    # Whole trajectories (untimed for `value`): samples per second.
+    traj_ms = run.trajectory_ms(1)
+
     # Full and cached steps timed apart (untimed for `value`): repeated full
     # steps from a trajectory start, and repeated cached steps at the
     # schedule's largest quota (its smallest active set).
     state.reset()
-    x.copy_(x_T_dev)
-    state.set_cond(cond_dev)
+    x.copy_(run.x_T_dev)
+    state.set_cond(run.cond_dev)
     full_ms = _event_time_ms(torch, lambda: state.full_step(x, float(times[0]), float(times[1])), 10)
     guided_full_ms = _event_time_ms(torch, lambda: state.guided_step(x, float(times[0]), float(times[1]), None,
                                                                      w.guidance), 10) if any(guided) else None
@@ -410,22 +479,21 @@ def main():
             state.profile_reset()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record()
-            n_act = run_step(k)
+            n_act = run.step(k)
             e1.record()
             e1.synchronize()
             cls = state.profile_read()
             rec = {"k": k + 1, "t": float(times[k]), "t_next": float(times[k + 1]),
                    "n_cache": quotas[k].tolist(), "n_active": int(n_act), "guided": bool(guided[k]),
-                   "model_flops": (2 if guided[k] else 1) * sum(f3c.forward_flops(cfg, cfg.tokens - int(c), 1)
-                                                                 for c in quotas[k]),
-                   "wall_ms": round(e0.elapsed_time(e1), 4),
+                   "model_flops": run.step_flops(k), "wall_ms": round(e0.elapsed_time(e1), 4),
                    "class_ms": {c: round(v["ms"], 4) for c, v in cls.items() if v["launches"]}}
             print(json.dumps(rec), file=sys.stderr, flush=True)
         state.profile(False)
 
     peak = PEAK_BF16_TFLOPS if cfg.dtype == "bf16" else PEAK_F32_TFLOPS
     achieved = prof["flops"] / (prof["ms"] * 1e-3) / 1e12 if prof["ms"] > 0 else 0.0
-    traffic, traffic_src = counter_traffic(dominant, w.name)
+    timed_ks = [i % T + 1 for i in range(args.steps)]
+    traffic, traffic_src = counter_traffic(dominant, w.name, timed_ks)
     roofline = {
         "bound": "mfma",
         "kernel": dominant,
@@ -441,6 +509,7 @@ def main():
         "launches": prof["launches"],
         "avg_launch_us": round(prof["ms"] * 1e3 / max(prof["launches"], 1), 2),
         "flops_per_launch": prof["flops"] / max(prof["launches"], 1),
+        "over": f"the {prof['launches']} launches of the timed steps (k = {timed_ks[0]}..{timed_ks[-1]})",
     }
     step_tflops = flop_total / elapsed / 1e12
     out = {
@@ -461,7 +530,8 @@ def main():
                    "steps_per_trajectory": T, "quota": w.schedule, "parallelism": "single GPU",
                    **({"guidance": w.guidance, "guided_steps": int(sum(guided))} if any(guided) else {})},
         "active_tokens_per_s": round(active / elapsed, 1),
-        "samples_per_s": round(w.batch * args.steps / elapsed / T, 3),
+        "trajectory_ms": round(traj_ms, 3),
+        "samples_per_s": round(w.batch * 1e3 / traj_ms, 4),
         "full_step_ms": round(full_ms, 4),
         **({"guided_full_step_ms": round(guided_full_ms, 4)} if guided_full_ms is not None else {}),
         "cached_step_ms": round(cached_ms, 4) if cached_ms is not None else None,
@@ -470,9 +540,23 @@ def main():
         "step_mfma_frac": round(step_tflops / peak, 4),
         "roofline": roofline,
     }
+    W_host, cond_host, x_T_host = run.W, run.cond, run.x_T
+    if args.secondary and args.secondary != w.name:
+        del run, state, x
+        torch.cuda.empty_cache()
+        r2 = Runner(args.secondary)
+        r2.trajectory_ms(1)                         # warm-up trajectory
+        ms2 = r2.trajectory_ms(2)
+        fl2 = sum(r2.step_flops(i) for i in range(r2.T))
+        out["secondary"] = {"workload": r2.w.name, "steps_per_s": round(r2.T * 1e3 / ms2, 3),
+                            "ms_per_step": round(ms2 / r2.T, 4), "trajectory_ms": round(ms2, 3),
+                            "step_model_tflops": round(fl2 / (ms2 * 1e-3) / 1e12, 2),
+                            "timed": "two whole trajectories after one warm-up trajectory"}
+        print(f"[bench] secondary {r2.w.name}: {ms2:.1f} ms per trajectory", file=sys.stderr, flush=True)
+        del r2
     if not args.no_cpu:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(w, W, cond, x_T, quotas, times, args.cpu_depth,
+        out["cpu_baseline"] = cpu_baseline(w, W_host, cond_host, x_T_host, quotas, times, args.cpu_depth,
                                            guided if any(guided) else None)
     print(json.dumps(out), flush=True)
 

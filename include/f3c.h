@@ -355,8 +355,14 @@ int f3c_op_dynamic_voxels(int32_t batch, int64_t n_words, const uint32_t* occ_ne
  * eta = 1 is uniform). out_host receives T+1 doubles. */
 int f3c_time_grid(int32_t steps, double eta, double* out_host);
 
-/* ceil(steps * rho) for a decimal ratio rho (anchor step with rho_a, guidance-off
- * step with rho_CFG-OFF). */
+/* ceil(steps * rho) for a decimal ratio rho (Algorithm 1: the anchor step
+ * ceil(T rho_a) ending Phase 1 and the step ceil(T rho_CFG-OFF) starting
+ * Phase 3). The paper gives the ratios as decimals, so rho stands for the
+ * shortest decimal that rounds to the double (0.2 is 1/5 exactly,
+ * 0.2000000001 is 2000000001 / 10^10) and the ceiling is exact on it, in
+ * integer arithmetic: f3c_ceil_ratio(25, 0.2) = 5, f3c_ceil_ratio(25,
+ * 0.2000000001) = 6. steps <= 0, rho <= 0 or NaN give 0; results above
+ * INT32_MAX saturate. */
 int32_t f3c_ceil_ratio(int32_t steps, double rho);
 
 /* Whether a step starting at time t is guided: 1 when lo <= t <= hi (the
@@ -370,7 +376,8 @@ int32_t f3c_pcsc_quota(int32_t k, int32_t n_tokens, double sigma, double mu, int
 /* Algorithm 1, step 1: cached count for step k (1-based): 0 in Phase 1
  * (k <= ceil(T rho_a)); n_cache_phase2 in Phase 2 (k < ceil(T rho_off));
  * in Phase 3, 0 when (k - ceil(T rho_off) + 1) mod f_corr == 0 (f_corr > 0),
- * else floor(N * xi). */
+ * else floor(N * xi). The ratios are read as decimals and the ceilings and
+ * the floor are exact, as in f3c_ceil_ratio. */
 int32_t f3c_phase_quota(int32_t k, int32_t steps, int32_t n_tokens, int32_t n_cache_phase2, double rho_a,
                         double rho_off, double xi, int32_t f_corr);
 

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <climits>
+#include <cstdlib>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -1018,10 +1020,98 @@ int f3c_time_grid(int32_t steps, double eta, double* out_host) {
 
 int32_t f3c_guidance_active(double t, double lo, double hi) { return (lo <= t && t <= hi) ? 1 : 0; }
 
-int32_t f3c_ceil_ratio(int32_t steps, double rho) {
-  const double p = steps * rho;
-  return (int32_t)std::ceil(p - 1e-9 * (p > 1 ? p : 1));
+// The schedule's ratios (rho_a, rho_CFG-OFF, xi) are decimals in the paper
+// (0.2, 0.75, 0.7). A double argument stands for the shortest decimal that
+// rounds to it (0.2 means 1/5 exactly, 0.2000000001 means 2000000001/10^10),
+// and the ceilings and floors of Algorithm 1 are taken exactly on that
+// decimal, in integer arithmetic.
+namespace {
+
+struct Decimal {
+  uint64_t mant;   // value = mant * 10^exp10
+  int exp10;
+};
+
+// Digit string of `prec` significant digits -> (mantissa, exponent), from
+// the "%.*e" form d.ddde[+-]xx of a positive finite value.
+bool parse_sci(const char* buf, Decimal* out) {
+  uint64_t m = 0;
+  int digits_after_point = 0, seen_point = 0;
+  const char* p = buf;
+  for (; *p && *p != 'e'; ++p) {
+    if (*p == '.') { seen_point = 1; continue; }
+    if (*p < '0' || *p > '9') return false;
+    m = m * 10 + (uint64_t)(*p - '0');
+    digits_after_point += seen_point;
+  }
+  if (*p != 'e') return false;
+  out->mant = m;
+  out->exp10 = std::atoi(p + 1) - digits_after_point;
+  return true;
 }
+
+// The shortest decimal that rounds to x (x > 0, finite), and among those of
+// that length the one nearest to x: the decimal a shortest round-trip
+// printer (such as Python's repr) produces.
+Decimal shortest_decimal(double x) {
+  char buf[64];
+  for (int prec = 1; prec <= 17; ++prec) {
+    std::snprintf(buf, sizeof buf, "%.*e", prec - 1, x);
+    if (std::strtod(buf, nullptr) == x) {
+      Decimal d{};
+      parse_sci(buf, &d);
+      return d;
+    }
+    // The nearest prec-digit decimal may fall just outside x's rounding
+    // interval while its neighbour one unit above or below lies inside (the
+    // interval is lopsided at powers of two). Try both, nearest first.
+    Decimal r{};
+    if (!parse_sci(buf, &r)) continue;
+    Decimal best{};
+    double best_dist = -1.0;
+    for (int dir = -1; dir <= 1; dir += 2) {
+      if (dir < 0 && r.mant == 0) continue;
+      const uint64_t mm = r.mant + (uint64_t)(int64_t)dir;
+      char cand[64];
+      std::snprintf(cand, sizeof cand, "%llue%d", (unsigned long long)mm, r.exp10);
+      const double v = std::strtod(cand, nullptr);
+      if (v != x) continue;
+      const long double dist = std::fabs((long double)mm * std::pow(10.0L, r.exp10) - (long double)x);
+      if (best_dist < 0 || dist < best_dist) {
+        best_dist = (double)dist;
+        best = Decimal{mm, r.exp10};
+      }
+    }
+    if (best_dist >= 0) return best;
+  }
+  Decimal d{};
+  std::snprintf(buf, sizeof buf, "%.16e", x);
+  parse_sci(buf, &d);
+  return d;
+}
+
+// floor(n * x) (or ceil) for 0 <= n < 2^31 and x >= 0 read as its shortest
+// decimal, exactly; results above INT32_MAX saturate there.
+int64_t scaled_round(int64_t n, double x, bool ceil_it) {
+  if (n <= 0 || !(x > 0.0)) return 0;
+  if (!std::isfinite(x)) return INT32_MAX;
+  const Decimal d = shortest_decimal(x);
+  unsigned __int128 num = (unsigned __int128)n * d.mant;
+  if (d.exp10 >= 0) {
+    for (int i = 0; i < d.exp10 && num <= INT32_MAX; ++i) num *= 10;
+    return num > INT32_MAX ? INT32_MAX : (int64_t)num;
+  }
+  // n * mant < 2^31 * 10^17 < 10^27: a divisor of 10^28 or more leaves 0.
+  if (-d.exp10 >= 28) return ceil_it ? (num > 0 ? 1 : 0) : 0;
+  unsigned __int128 den = 1;
+  for (int i = 0; i < -d.exp10; ++i) den *= 10;
+  const unsigned __int128 q = num / den + (ceil_it && num % den != 0 ? 1 : 0);
+  return q > INT32_MAX ? INT32_MAX : (int64_t)q;
+}
+
+}  // namespace
+
+int32_t f3c_ceil_ratio(int32_t steps, double rho) { return (int32_t)scaled_round(steps, rho, true); }
 
 int32_t f3c_pcsc_quota(int32_t k, int32_t n_tokens, double sigma, double mu, int32_t k_anchor, double gamma_up) {
   const double bound = n_tokens - sigma * std::exp(mu * (k - k_anchor)) / gamma_up;
@@ -1038,8 +1128,7 @@ int32_t f3c_phase_quota(int32_t k, int32_t steps, int32_t n_tokens, int32_t n_ca
   if (k < k_off) return n_cache_phase2;
   const int32_t k_refine = k - k_off;
   if (f_corr > 0 && (k_refine + 1) % f_corr == 0) return 0;
-  const double p = n_tokens * xi;
-  return (int32_t)std::floor(p + 1e-9 * (p > 1 ? p : 1));
+  return (int32_t)scaled_round(n_tokens, xi, false);
 }
 
 int32_t f3c_tau_forces_full(int32_t consecutive, int32_t tau, int32_t reading) {

@@ -8,6 +8,7 @@
 """
 import ctypes
 import math
+import os
 import subprocess
 
 import numpy as np
@@ -181,6 +182,44 @@ def test_ceil_ratio_and_phase_rule_match_oracle():
                         osched.phase_quota(k, T, 4096, 1234, 0.2, 0.75, xi, f_corr)
 
 
+def test_ceil_ratio_is_exact_on_decimals():
+    # ratios are decimals: a ratio a hair above a fraction that lands on an
+    # integer must take the next integer, exactly as the oracle's exact ceiling
+    assert f3c.ceil_ratio(25, 0.2) == osched.ceil_ratio(25, 0.2) == 5
+    assert f3c.ceil_ratio(25, 0.2000000001) == osched.ceil_ratio(25, 0.2000000001) == 6
+    assert f3c.ceil_ratio(10, 0.30000000001) == osched.ceil_ratio(10, 0.30000000001) == 4
+    assert f3c.ceil_ratio(25, 0.7599999999999999) == osched.ceil_ratio(25, 0.7599999999999999) == 19
+    assert f3c.ceil_ratio(25, 0.76) == osched.ceil_ratio(25, 0.76) == 19
+    assert f3c.ceil_ratio(25, 0.0) == 0 and f3c.ceil_ratio(0, 0.5) == 0
+    assert f3c.ceil_ratio(25, 5e-324) == osched.ceil_ratio(25, 5e-324) == 1
+    rng = np.random.default_rng(7)
+    cases = [float(v) for v in rng.random(3000)]
+    cases += [round(float(v), int(p)) for v, p in zip(rng.random(3000), rng.integers(1, 17, 3000))]
+    cases += [2.0 ** -e for e in range(1, 60)] + [1.0 - 2.0 ** -e for e in range(1, 53)]
+    cases += [np.nextafter(v, 1.0) for v in (0.2, 0.25, 0.3, 0.75, 0.7)]
+    cases += [np.nextafter(v, 0.0) for v in (0.2, 0.25, 0.3, 0.75, 0.7)]
+    for rho in cases:
+        for T in (1, 7, 25, 1000, 2 ** 31 - 1):
+            assert f3c.ceil_ratio(T, rho) == min(osched.ceil_ratio(T, rho), 2 ** 31 - 1), (T, rho)
+
+
+def test_phase_quota_floor_is_exact_on_decimals():
+    # N * xi just below and at an integer: the floor of the exact decimal product
+    k3 = 20                                   # a Phase 3 step at T = 25, no correction with f_corr = 0
+    for N, xi in [(32768, 0.7), (4096, 0.7), (10, 0.3), (10, 0.29999999999), (10, 0.30000000001),
+                  (3, 1.0 / 3.0), (1000, 0.0009999999999999998), (1000, 0.001), (7, 0.9999999999999999)]:
+        got = f3c.phase_quota(k3, 25, N, 0, 0.2, 0.75, xi, 0)
+        want = osched.phase_quota(k3, 25, N, 0, 0.2, 0.75, xi, 0)
+        assert got == want, (N, xi, got, want)
+    assert f3c.phase_quota(k3, 25, 10, 0, 0.2, 0.75, 0.29999999999, 0) == 2
+    assert f3c.phase_quota(k3, 25, 10, 0, 0.2, 0.75, 0.3, 0) == 3
+    rng = np.random.default_rng(11)
+    for xi in [round(float(v), int(p)) for v, p in zip(rng.random(2000), rng.integers(1, 17, 2000))]:
+        for N in (512, 4096, 32768):
+            assert f3c.phase_quota(k3, 25, N, 0, 0.2, 0.75, xi, 0) == osched.phase_quota(k3, 25, N, 0, 0.2, 0.75,
+                                                                                         xi, 0), (N, xi)
+
+
 def test_pcsc_quota_matches_oracle():
     for N in (512, 4096, 32768):
         for sigma in (0.0, 100.0, 6400.0, 2e5, 1e9):
@@ -206,15 +245,33 @@ def test_driver_is_built_and_checks_arguments():
         assert r.returncode == 1 and msg in r.stderr, (args, r.stderr)
 
 
-def test_bench_counter_traffic_lookup():
+def test_bench_counter_traffic_lookup(tmp_path, monkeypatch):
     import bench
-    v, why = bench.counter_traffic("attn_self", "trellis32_cached")
-    assert v is None and "only" in why
-    v, why = bench.counter_traffic("no_such_class", "trellis16_cached")
-    assert v is None
-    v, why = bench.counter_traffic("attn_self", "trellis16_cached")
-    # a figure while the kernel sources match the recorded hash, else a stated reason
-    assert (isinstance(v, int) and v > 0) or (v is None and "changed" in why)
+    v, why = bench.counter_traffic("attn_self", "no_such_workload", [1])
+    assert v is None and "no counter summary" in why
+    # a planted summary: per-step lines, averaged over the timed steps' launches
+    import hashlib
+    csrc = os.path.join(bench.ROOT, "paper_2511_22533_amd", "csrc")
+    digest = hashlib.sha256(open(os.path.join(csrc, "k_attn.hip"), "rb").read()).hexdigest()
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    lines = [f"traffic attn_self k={k}: {1000 * k} bytes over 2 calls; sources k_attn.hip sha256 {digest}"
+             for k in (1, 2, 3)]
+    (prof / "demo_traffic.md").write_text("\n".join(lines) + "\n")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    os.makedirs(tmp_path / "paper_2511_22533_amd", exist_ok=True)
+    os.symlink(csrc, tmp_path / "paper_2511_22533_amd" / "csrc")
+    v, why = bench.counter_traffic("attn_self", "demo", [1, 2, 3])
+    assert v == round((1000 + 2000 + 3000) / 6)
+    v, why = bench.counter_traffic("attn_self", "demo", [3, 3])
+    assert v == 1500
+    v, why = bench.counter_traffic("attn_self", "demo", [4])
+    assert v is None and "every timed step" in why
+    v, why = bench.counter_traffic("gemm_o", "demo", [1])
+    assert v is None and "no counter line" in why
+    (prof / "demo_traffic.md").write_text(lines[0].replace(digest, "0" * 64) + "\n")
+    v, why = bench.counter_traffic("attn_self", "demo", [1])
+    assert v is None and "changed" in why
 
 
 @pytest.mark.parametrize("steps", [10, 25, 50])

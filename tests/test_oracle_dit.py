@@ -40,6 +40,19 @@ def test_gelu_tanh_identities():
     assert abs(dit.gelu_tanh(np.array([30.0]))[0] - 30.0) < 1e-12
 
 
+def test_gelu_tanh_approximates_exact_gelu():
+    # The tanh form approximates GELU(x) = x * Phi(x), with Phi the standard
+    # normal CDF written through math.erf, to within 4.8e-4 on [-8, 8]. A bound
+    # of 5e-4 rejects the plausible slips: a cubic coefficient of 0.04 or 0.05
+    # (2.9e-3, 3.0e-3), a dropped cubic term (3.4e-2), sqrt(1/pi) for sqrt(2/pi)
+    # (0.10), or the sigmoid form x * sigmoid(1.702 x) (2.0e-2).
+    x = np.linspace(-8.0, 8.0, 16001)
+    exact = np.array([v * 0.5 * (1.0 + math.erf(v / math.sqrt(2.0))) for v in x])
+    err = np.max(np.abs(dit.gelu_tanh(x) - exact))
+    assert err < 5e-4, err
+    assert err > 4e-4, err      # the tanh form, not the exact one
+
+
 def test_silu_closed_form():
     assert dit.silu(np.array([0.0]))[0] == 0.0
     assert np.isclose(dit.silu(np.array([1.0]))[0], 1.0 / (1.0 + math.exp(-1.0)))
