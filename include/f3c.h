@@ -205,10 +205,14 @@ int f3c_guided_step(f3c_state* s, float* x_dev, double t, double t_next, const i
                     f3c_stream stream);
 
 /* Device views of the state (valid until the next step call):
- * v_cache / v_prev float32 [B][N][8]; idx_active int32 [sum n_b]; pos int32
- * [B][N] (packed active row or -1); v_act float32 [sum n_b][8]; mod float32
- * [L][6][width]; score float32 [B][N] (written only while score recording is
- * on). act_off_host receives the B+1 active-row offsets of the last step. */
+ * v_cache / v_prev float32 [B][N][8]; idx_active int32 [sum n_b] and pos int32
+ * [B][N] (packed active row or -1) of the last step's selection, both NULL
+ * when the last step selected nothing (every c_b == 0: every token active in
+ * token order); v_act float32 [sum n_b][8]; mod float32 [L][6][width], the
+ * modulation vectors the last step read (its planned vectors when its time was
+ * planned; valid while that plan is); score float32 [B][N] (written only while
+ * score recording is on). act_off_host receives the B+1 active-row offsets of
+ * the last step. */
 int f3c_state_views(const f3c_state* s, float** v_cache, float** v_prev, int32_t** idx_active, int32_t** pos,
                     float** v_act, float** mod, float** score, int32_t* act_off_host);
 int f3c_state_record_scores(f3c_state* s, int32_t on);
@@ -221,6 +225,36 @@ int f3c_state_record_scores(f3c_state* s, int32_t on);
  * F3C_ENOMEM before enqueuing anything. NULL turns it off. It serves the
  * per-block parity of the transformer (the change each block makes to h). */
 int f3c_state_trace_blocks(f3c_state* s, float* h_trace_dev, size_t bytes);
+
+/* Debug: while sub_trace_dev is set (device, 16-byte aligned, bytes long),
+ * every step also writes the outputs of each block's three sublayers before
+ * they enter the residual stream, float32 [L][3][rows][width] (rows as for
+ * f3c_state_trace_blocks): slice 3l is the self-attention output after its
+ * output projection and bias, before the gate of the adaLN modulation; slice
+ * 3l + 1 the cross-attention output after its projection and bias (it has no
+ * gate); slice 3l + 2 the MLP output after the second linear and its bias,
+ * before its gate (the block of Sec. 3.2 with the supplement's FLOPs list:
+ * h += g1 * SA, h += CA, h += g2 * MLP). Each slice comes from the step's own
+ * projection kernel run a second time, ungated, into the zeroed slice, so it
+ * is the value the step adds. A step whose slices do not fit fails with
+ * F3C_ENOMEM before enqueuing anything. NULL turns it off. */
+int f3c_state_trace_sublayers(f3c_state* s, float* sub_trace_dev, size_t bytes);
+
+/* Debug, teacher forcing of the selection (Algorithm 1: the active set I_active
+ * that SSC chooses; Sec. 4.2, the transformer runs on x[:, I_active, :]): the
+ * next step call of this state takes its active sets from idx_active_dev
+ * (device int32, 4-byte aligned) instead of scoring and selecting them. For
+ * sample b with cached count c_b its N - c_b active tokens are rows act_off[b]
+ * .. act_off[b+1] - 1 (act_off the running sum of N - c_b from 0), ascending
+ * token indices in [0, N); a sample with c_b == 0 lists 0 .. N-1. The step
+ * copies them into the state (the idx_active view), builds pos from them and
+ * consumes the hook; a step with every c_b == 0 consumes it without reading
+ * the buffer. The buffer must stay valid until that step's work on its stream
+ * has run. Entries outside [0, N) are clamped into range, so no access leaves
+ * the state's arrays (the step's result is then unspecified); other contract
+ * violations (not ascending, duplicates) also give unspecified results.
+ * NULL disarms. Errors: F3C_EINVAL (NULL state, misaligned buffer). */
+int f3c_debug_force_active(f3c_state* s, const int32_t* idx_active_dev);
 
 /* Checkpoint: the sampler state beyond x is the cache pair. export copies
  * v_cache then v_prev (2*B*N*8 floats) to host memory; import restores them.

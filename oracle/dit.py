@@ -27,9 +27,12 @@ All linear weights are stored [out][in] and applied as y = x W^T + b.
 from __future__ import annotations
 
 import math
+import os
+from concurrent.futures import ThreadPoolExecutor
 from typing import Dict
 
 import numpy as np
+from threadpoolctl import threadpool_limits
 
 F64 = np.float64
 LN_EPS = 1e-6
@@ -68,22 +71,36 @@ def timestep_features(t: float, n_freq: int = 256) -> np.ndarray:
 
 
 def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, heads: int) -> np.ndarray:
-    """Multi-head softmax attention: q [n][d], k/v [m][d] -> [n][d] (heads split along d)."""
+    """Multi-head softmax attention: q [n][d], k/v [m][d] -> [n][d] (heads split along d).
+
+    Per head: S = Q K^T / sqrt(d_head); P = exp(S - rowmax(S)) / rowsum(...);
+    O = P V, with the query rows taken QUERY_CHUNK at a time (the scores of
+    one chunk are materialised in full). The heads are independent, so they
+    run concurrently on threads, each with a one-thread BLAS; every head's
+    arithmetic is the same sequence of whole-array operations as in a serial
+    loop (done in place on the chunk's score array), so the result does not
+    depend on the thread count."""
     n, d = q.shape
     hd = d // heads
     out = np.empty((n, d), dtype=F64)
     scale = 1.0 / math.sqrt(hd)
-    for h in range(heads):
+
+    def one_head(h: int) -> None:
         sl = slice(h * hd, (h + 1) * hd)
         kh_t = np.ascontiguousarray(k[:, sl].T)
         vh = v[:, sl]
         for q0 in range(0, n, QUERY_CHUNK):
             qh = q[q0:q0 + QUERY_CHUNK, sl]
-            s = _matmul(qh, kh_t) * scale
-            s = s - s.max(axis=1, keepdims=True)
-            p = np.exp(s)
-            p = p / p.sum(axis=1, keepdims=True)
-            out[q0:q0 + QUERY_CHUNK, sl] = _matmul(p, vh)
+            s = _matmul(qh, kh_t)
+            np.multiply(s, scale, out=s)
+            np.subtract(s, s.max(axis=1, keepdims=True), out=s)
+            np.exp(s, out=s)
+            np.divide(s, s.sum(axis=1, keepdims=True), out=s)
+            out[q0:q0 + QUERY_CHUNK, sl] = _matmul(s, vh)
+
+    workers = max(1, min(heads, len(os.sched_getaffinity(0))))
+    with threadpool_limits(limits=1, user_api="blas"), ThreadPoolExecutor(workers) as ex:
+        list(ex.map(one_head, range(heads)))
     return out
 
 
@@ -114,22 +131,41 @@ class Model:
         w = self.w
         return linear(np.asarray(x_active, dtype=F64), w["in_w"], w["in_b"]) + w["pos"][idx]
 
-    def block(self, l: int, h: np.ndarray, mod_l: np.ndarray, cond_k: np.ndarray,
-              cond_v: np.ndarray, trace: dict | None = None) -> np.ndarray:
+    def self_attention_sublayer(self, l: int, h: np.ndarray, mod_l: np.ndarray) -> np.ndarray:
+        """SA(LN(h)(1+scale1)+shift1) after its output projection, before the gate g1."""
         w, heads, d = self.w, self.cfg.heads, self.cfg.width
         p = f"blk{l}."
-        sh1, sc1, g1, sh2, sc2, g2 = mod_l
+        sh1, sc1 = mod_l[0], mod_l[1]
         u = layer_norm(h) * (1.0 + sc1) + sh1
         qkv = linear(u, w[p + "qkv_w"], w[p + "qkv_b"])
         sa = attention(qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:], heads)
-        sa_out = linear(sa, w[p + "o_w"], w[p + "o_b"])
-        h = h + g1 * sa_out
+        return linear(sa, w[p + "o_w"], w[p + "o_b"])
+
+    def cross_attention_sublayer(self, l: int, h: np.ndarray, cond_k: np.ndarray,
+                                 cond_v: np.ndarray) -> np.ndarray:
+        """CA(LN(h), cond) after its output projection (no gate)."""
+        w, heads = self.w, self.cfg.heads
+        p = f"blk{l}."
         q = linear(layer_norm(h), w[p + "q_w"], w[p + "q_b"])
         ca = attention(q, cond_k, cond_v, heads)
-        ca_out = linear(ca, w[p + "co_w"], w[p + "co_b"])
-        h = h + ca_out
+        return linear(ca, w[p + "co_w"], w[p + "co_b"])
+
+    def mlp_sublayer(self, l: int, h: np.ndarray, mod_l: np.ndarray) -> np.ndarray:
+        """MLP(LN(h)(1+scale2)+shift2) after the second linear, before the gate g2."""
+        w = self.w
+        p = f"blk{l}."
+        sh2, sc2 = mod_l[3], mod_l[4]
         u = layer_norm(h) * (1.0 + sc2) + sh2
-        mlp = linear(gelu_tanh(linear(u, w[p + "fc1_w"], w[p + "fc1_b"])), w[p + "fc2_w"], w[p + "fc2_b"])
+        return linear(gelu_tanh(linear(u, w[p + "fc1_w"], w[p + "fc1_b"])), w[p + "fc2_w"], w[p + "fc2_b"])
+
+    def block(self, l: int, h: np.ndarray, mod_l: np.ndarray, cond_k: np.ndarray,
+              cond_v: np.ndarray, trace: dict | None = None) -> np.ndarray:
+        g1, g2 = mod_l[2], mod_l[5]
+        sa_out = self.self_attention_sublayer(l, h, mod_l)
+        h = h + g1 * sa_out
+        ca_out = self.cross_attention_sublayer(l, h, cond_k, cond_v)
+        h = h + ca_out
+        mlp = self.mlp_sublayer(l, h, mod_l)
         h = h + g2 * mlp
         if trace is not None:
             trace[l] = {"sa_out": sa_out, "ca_out": ca_out, "mlp_out": mlp, "h": h.copy()}

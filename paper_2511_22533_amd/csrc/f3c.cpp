@@ -103,6 +103,11 @@ struct f3c_state {
   float* plan_mod = nullptr;
   float* trace = nullptr;       // debug: residual stream after the embedding and after each block
   size_t trace_bytes = 0;
+  float* sub_trace = nullptr;   // debug: pre-gate sublayer outputs of each block
+  size_t sub_trace_bytes = 0;
+  const int32_t* force_idx = nullptr;   // debug: the next step's active sets (teacher forcing)
+  const float* last_mod = nullptr;      // modulation vectors the last step read
+  bool last_selected = false;           // the last step wrote idx/pos (some sample cached)
   bool cond_set = false, uncond_set = false, record_scores = false;
   uint32_t prof_mask = 0;
   float omega = 0.7f;
@@ -239,7 +244,13 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
   const int32_t* idx = nullptr;
   const int32_t* pos = nullptr;
 
-  if (any_cached) {
+  const int32_t* forced = s->force_idx;
+  s->force_idx = nullptr;                   // a step consumes the hook
+  if (any_cached && forced) {
+    HIP_TRY(launch_force_active(forced, act, N, s->idx, s->pos, st));
+    idx = s->idx;
+    pos = s->pos;
+  } else if (any_cached) {
     const float w_a = s->omega, w_v = 1.0f - w_a;
     Scope sc(s, F3C_PROF_SELECT, st, 0, (double)B * N * (64 + 4) + arows * 4.0);
     HIP_TRY(launch_select(v_cache, v_prev, B, N, w_a, w_v, quota, act, s->idx, s->pos,
@@ -304,6 +315,12 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
         HIP_TRY(launch_gemm(SITE_O, dt, EPI_RESID, rows, d, d, s->att, d, m->w(bw.o_w), d, m->b(bw.o_b), md + 2 * d,
                             nullptr, 0, s->h, d, st));
       }
+      if (s->sub_trace) {   // the same projection into a zeroed slice, without the gate
+        float* sl = s->sub_trace + (size_t)(3 * l) * hslice;
+        HIP_TRY(launch_zero(sl, hslice * 4, st));
+        HIP_TRY(launch_gemm(SITE_OP, dt, EPI_RESID, rows, d, d, s->att, d, m->w(bw.o_w), d, m->b(bw.o_b), nullptr,
+                            nullptr, 0, sl, d, st));
+      }
       {
         Scope sc(s, F3C_PROF_LN, st, 0, lnb);
         HIP_TRY(launch_ln_mod(dt, s->h, rows, d, nullptr, nullptr, s->u, st));
@@ -324,6 +341,12 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
         HIP_TRY(launch_gemm(SITE_CO, dt, EPI_RESID, rows, d, d, s->att, d, m->w(bw.co_w), d, m->b(bw.co_b), nullptr,
                             nullptr, 0, s->h, d, st));
       }
+      if (s->sub_trace) {
+        float* sl = s->sub_trace + (size_t)(3 * l + 1) * hslice;
+        HIP_TRY(launch_zero(sl, hslice * 4, st));
+        HIP_TRY(launch_gemm(SITE_OP, dt, EPI_RESID, rows, d, d, s->att, d, m->w(bw.co_w), d, m->b(bw.co_b), nullptr,
+                            nullptr, 0, sl, d, st));
+      }
       {
         Scope sc(s, F3C_PROF_LN, st, 0, lnb);
         HIP_TRY(launch_ln_mod(dt, s->h, rows, d, md + 3 * d, md + 4 * d, s->u, st));
@@ -337,6 +360,12 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
         Scope sc(s, F3C_PROF_GEMM_FC2, st, 2.0 * rows * d * dm, proj_bytes(dd, dm, true));
         HIP_TRY(launch_gemm(SITE_FC2, dt, EPI_RESID, rows, d, dm, s->hid, dm, m->w(bw.fc2_w), dm, m->b(bw.fc2_b),
                             md + 5 * d, nullptr, 0, s->h, d, st));
+      }
+      if (s->sub_trace) {
+        float* sl = s->sub_trace + (size_t)(3 * l + 2) * hslice;
+        HIP_TRY(launch_zero(sl, hslice * 4, st));
+        HIP_TRY(launch_gemm(SITE_OP, dt, EPI_RESID, rows, d, dm, s->hid, dm, m->w(bw.fc2_w), dm, m->b(bw.fc2_b), nullptr,
+                            nullptr, 0, sl, d, st));
       }
       if (s->trace)
         HIP_TRY(hipMemcpyAsync(s->trace + (l + 1) * hslice, s->h, hslice * 4, hipMemcpyDeviceToDevice, st));
@@ -355,6 +384,8 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
   }
   s->cur = 1 - s->cur;
   s->last_act = act;
+  s->last_mod = mod;
+  s->last_selected = pos != nullptr;
   return F3C_OK;
 }
 
@@ -725,11 +756,15 @@ static int step_common(f3c_state* s, float* x, double t, double t_next, const in
     for (int b = 0; b < s->B; ++b)
       if (n_cache[b] < 0 || n_cache[b] > s->m->N)
         return fail(F3C_EINVAL, "n_cache[%d] = %d outside [0, %d]", b, n_cache[b], s->m->N);
-  if (s->trace) {
+  if (s->trace || s->sub_trace) {
     size_t rows = 0;
     for (int b = 0; b < s->B; ++b) rows += s->m->N - (n_cache ? n_cache[b] : 0);
-    const size_t need = (size_t)(s->m->L + 1) * rows * (guide ? 2 : 1) * s->m->d * sizeof(float);
-    if (need > s->trace_bytes) return fail(F3C_ENOMEM, "trace buffer %zu < %zu bytes", s->trace_bytes, need);
+    const size_t slice = rows * (guide ? 2 : 1) * s->m->d * sizeof(float);
+    if (s->trace && (size_t)(s->m->L + 1) * slice > s->trace_bytes)
+      return fail(F3C_ENOMEM, "trace buffer %zu < %zu bytes", s->trace_bytes, (size_t)(s->m->L + 1) * slice);
+    if (s->sub_trace && (size_t)(3 * s->m->L) * slice > s->sub_trace_bytes)
+      return fail(F3C_ENOMEM, "sublayer trace buffer %zu < %zu bytes", s->sub_trace_bytes,
+                  (size_t)(3 * s->m->L) * slice);
   }
   if (guide) {
     if (!s->guided) return fail(F3C_ESTATE, "state was not created with F3C_STATE_GUIDED");
@@ -759,10 +794,10 @@ int f3c_state_views(const f3c_state* s, float** v_cache, float** v_prev, int32_t
   if (!s) return fail(F3C_EINVAL, "state is NULL");
   if (v_cache) *v_cache = s->v[s->cur];
   if (v_prev) *v_prev = s->v[1 - s->cur];
-  if (idx_active) *idx_active = s->idx;
-  if (pos) *pos = s->pos;
+  if (idx_active) *idx_active = s->last_selected ? s->idx : nullptr;
+  if (pos) *pos = s->last_selected ? s->pos : nullptr;
   if (v_act) *v_act = s->vact;
-  if (mod) *mod = s->mod;
+  if (mod) *mod = const_cast<float*>(s->last_mod ? s->last_mod : s->mod);
   if (score) *score = s->score;
   if (act_off_host)
     for (int b = 0; b <= s->B; ++b) act_off_host[b] = s->last_act.off[b];
@@ -774,6 +809,21 @@ int f3c_state_trace_blocks(f3c_state* s, float* h_trace_dev, size_t bytes) {
   if (h_trace_dev && ((uintptr_t)h_trace_dev & 15)) return fail(F3C_EINVAL, "trace buffer must be 16-byte aligned");
   s->trace = h_trace_dev;
   s->trace_bytes = h_trace_dev ? bytes : 0;
+  return F3C_OK;
+}
+
+int f3c_state_trace_sublayers(f3c_state* s, float* trace_dev, size_t bytes) {
+  if (!s) return fail(F3C_EINVAL, "state is NULL");
+  if (trace_dev && ((uintptr_t)trace_dev & 15)) return fail(F3C_EINVAL, "trace buffer must be 16-byte aligned");
+  s->sub_trace = trace_dev;
+  s->sub_trace_bytes = trace_dev ? bytes : 0;
+  return F3C_OK;
+}
+
+int f3c_debug_force_active(f3c_state* s, const int32_t* idx_active_dev) {
+  if (!s) return fail(F3C_EINVAL, "state is NULL");
+  if (idx_active_dev && ((uintptr_t)idx_active_dev & 3)) return fail(F3C_EINVAL, "index buffer must be 4-byte aligned");
+  s->force_idx = idx_active_dev;
   return F3C_OK;
 }
 

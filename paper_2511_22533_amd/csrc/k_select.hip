@@ -243,7 +243,35 @@ __global__ __launch_bounds__(kThreads) void k_score_select(const float* __restri
   }
 }
 
+// Teacher-forced selection: pos of every token is -1 ...
+__global__ __launch_bounds__(256) void k_pos_fill(int32_t* __restrict__ pos, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) pos[i] = -1;
+}
+
+// ... then every listed row r of sample b sets idx_active[r] = i and
+// pos[b][i] = r, with i clamped into [0, N) so that no access leaves the
+// arrays whatever the caller's buffer holds.
+__global__ __launch_bounds__(256) void k_force_scatter(const int32_t* __restrict__ idx_in, Segs act, int N,
+                                                       int32_t* __restrict__ idx_out, int32_t* __restrict__ pos) {
+  const int r = blockIdx.x * 256 + threadIdx.x;
+  if (r >= act.off[act.B]) return;
+  const int b = find_segment(act.off, act.B, r);
+  const int i = min(max(idx_in[r], 0), N - 1);
+  idx_out[r] = i;
+  pos[(size_t)b * N + i] = r;
+}
+
 }  // namespace
+
+hipError_t launch_force_active(const int32_t* idx_in, const Segs& act, int N, int32_t* idx_out, int32_t* pos,
+                               hipStream_t s) {
+  const int64_t n = (int64_t)act.B * N;
+  launch(k_pos_fill, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, pos, n);
+  const int rows = act.off[act.B];
+  if (rows > 0) launch(k_force_scatter, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, s, idx_in, act, N, idx_out, pos);
+  return hipGetLastError();
+}
 
 hipError_t launch_select(const float* v_cache, const float* v_prev, int B, int N, float w_a, float w_v,
                          const Segs& n_cache, const Segs& act, int32_t* idx_active, int32_t* pos,

@@ -32,6 +32,11 @@ hipError_t launch_select(const float* v_cache, const float* v_prev, int B, int N
                          const Segs& n_cache, const Segs& act, int32_t* idx_active, int32_t* pos,
                          float* score, hipStream_t s);
 
+// Teacher-forced selection: idx_out[r] = idx_in[r] (clamped into [0, N)) for
+// the act.off[B] listed rows, pos[b][i] = r for listed tokens, -1 elsewhere.
+hipError_t launch_force_active(const int32_t* idx_in, const Segs& act, int N, int32_t* idx_out, int32_t* pos,
+                               hipStream_t s);
+
 // h[r][:] = x[b][i][:] W_in^T + b_in + P[i][:], i = idx_active[r] (identity when idx == nullptr);
 // with dup > 0 the row is also written to h[r + dup] (the unconditional pass of a guided step).
 hipError_t launch_embed(int dt, const float* x, int N, const int32_t* idx, const Segs& act,

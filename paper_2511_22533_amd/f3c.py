@@ -64,6 +64,8 @@ _SIGS = {
     "f3c_guided_step": (c_int, [c_p, c_p, c_d, c_d, P_i32, c_d, c_p]),
     "f3c_guidance_active": (c_int, [c_d, c_d, c_d]),
     "f3c_state_trace_blocks": (c_int, [c_p, c_p, c_sz]),
+    "f3c_state_trace_sublayers": (c_int, [c_p, c_p, c_sz]),
+    "f3c_debug_force_active": (c_int, [c_p, c_p]),
     "f3c_state_destroy": (None, [c_p]),
     "f3c_state_reset": (c_int, [c_p, c_p]),
     "f3c_state_set_omega": (c_int, [c_p, c_f]),
@@ -324,6 +326,16 @@ class State:
         """Debug: copy the residual stream after the embedding and each block into buf (f32 device tensor)."""
         check(lib().f3c_state_trace_blocks(self.h, _ptr(buf), buf.numel() * 4 if buf is not None else 0))
 
+    def trace_sublayers(self, buf=None):
+        """Debug: write each block's pre-gate sublayer outputs into buf (f32 device tensor [L][3][rows][width])."""
+        check(lib().f3c_state_trace_sublayers(self.h, _ptr(buf), buf.numel() * 4 if buf is not None else 0))
+
+    def force_active(self, idx_active=None):
+        """Debug: the next step uses these active sets (int32 device tensor, per sample ascending,
+        concatenated) instead of its own selection; None disarms."""
+        check(lib().f3c_debug_force_active(self.h, _ptr(idx_active)))
+        self._forced = idx_active          # kept alive until the step has run
+
     def record_scores(self, on: bool):
         check(lib().f3c_state_record_scores(self.h, int(on)))
 
@@ -344,12 +356,16 @@ class State:
         cfg, B = self.model.cfg, self.batch
         N = cfg.tokens
         rows = v["act_off"][-1]
-        base = self.buf.data_ptr()
 
         def view(ptr, n, dtype, shape):
-            off = ptr - base
+            if ptr is None:
+                return None
             nbytes = n * torch.empty((), dtype=dtype).element_size()
-            return self.buf[off:off + nbytes].view(dtype).view(shape)
+            for owner in (self.buf, self.plan_buf):   # the state's buffer, or the modulation plan's
+                if owner is not None and owner.data_ptr() <= ptr and ptr + nbytes <= owner.data_ptr() + owner.numel():
+                    off = ptr - owner.data_ptr()
+                    return owner[off:off + nbytes].view(dtype).view(shape)
+            raise F3CError(F3C_EINVAL, "view outside the state's buffers")
 
         return {
             "v_cache": view(v["v_cache"], B * N * 8, torch.float32, (B, N, 8)),

@@ -37,8 +37,13 @@ def _gpu_step(torch, pair, x_dev, t, tn, n_cache, w=None):
         pair.state.full_step(x_dev, t, tn)
     torch.cuda.synchronize()
     after = pair.state.tensors()
-    return dict(vc=vc, vp=vp, x0=x_before, x1=x_dev.cpu().numpy(), idx=after["idx_active"].cpu().numpy(),
-                pos=after["pos"].cpu().numpy(), vact=after["v_act"].cpu().numpy(), off=after["act_off"],
+    if any(n_cache):
+        idx, pos = after["idx_active"].cpu().numpy(), after["pos"].cpu().numpy()
+    else:   # a step without selection leaves no index views
+        assert after["idx_active"] is None and after["pos"] is None
+        idx = pos = None
+    return dict(vc=vc, vp=vp, x0=x_before, x1=x_dev.cpu().numpy(), idx=idx,
+                pos=pos, vact=after["v_act"].cpu().numpy(), off=after["act_off"],
                 vnew=after["v_cache"].cpu().numpy(), vold=after["v_prev"].cpu().numpy())
 
 
