@@ -173,7 +173,7 @@ def hbm_sweep():
                          "GB/s": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4)})
         print(f"[sweep] {kernel:12s} {shape:28s} {ms * 1e3:9.2f} us {gbs:8.1f} GB/s", file=sys.stderr, flush=True)
 
-    for B, N in [(1, 4096), (4, 4096), (16, 32768), (64, 32768)]:
+    for B, N in [(1, 4096), (4, 4096), (1, 32768), (16, 32768), (64, 32768)]:
         vc = torch.randn((B, N, 8), device="cuda", generator=g)
         vp = torch.randn((B, N, 8), device="cuda", generator=g)
         n_cache = [int(0.8 * N)] * B

@@ -296,9 +296,17 @@ int f3c_profile_reset(f3c_state* s);
 /* SSC scoring + selection (Eqs. 2, 6, 7; Algorithm 1 SSC) for B samples of N
  * tokens: v_cache, v_prev float32 [B][N][8]; n_cache_host[b] in [0, N]. Writes
  * idx_active (int32, sum(N - c_b) rows, ascending per sample), pos int32 [B][N]
- * and, if score != NULL, score float32 [B][N] (for samples with c_b > 0). */
+ * and, if score != NULL, score float32 [B][N] (for samples with c_b > 0).
+ * workspace: device scratch, 256-byte aligned, at least
+ * f3c_op_select_workspace_bytes(B, N) bytes (the per-token magnitudes and the
+ * partial extremes passed from the streaming scoring pass to the per-sample
+ * selection); caller-owned, contents undefined after the call. Errors:
+ * F3C_EINVAL (shapes, NULL or misaligned buffers, omega outside [0, 1]),
+ * F3C_ENOMEM (workspace too small). */
+int f3c_op_select_workspace_bytes(int32_t batch, int32_t n_tokens, size_t* bytes);
 int f3c_op_select(int32_t batch, int32_t n_tokens, const float* v_cache, const float* v_prev, float omega,
-                  const int32_t* n_cache_host, int32_t* idx_active, int32_t* pos, float* score, f3c_stream stream);
+                  const int32_t* n_cache_host, int32_t* idx_active, int32_t* pos, float* score, void* workspace,
+                  size_t workspace_bytes, f3c_stream stream);
 
 /* out/resid = A W^T + bias (+ epilogue). A: T [M][lda], W: T [N][ldw], bias f32 [N].
  * epilogue 0: out T [M][ldo] = value; 1: out = GELU_tanh(value);

@@ -96,6 +96,7 @@ struct f3c_state {
   float *h, *vact, *mod, *temb, *score;
   void *u, *qkv, *att, *qc, *hid, *cond_t, *kv;
   int32_t *idx, *pos;
+  void* sel_ws = nullptr;       // selection: magnitude pairs and partial extremes
   float* ws = nullptr;          // attention key-split partials
   size_t ws_bytes = 0;
   bool guided = false;          // activations and condition K/V sized for two passes per sample
@@ -254,7 +255,7 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
     const float w_a = s->omega, w_v = 1.0f - w_a;
     Scope sc(s, F3C_PROF_SELECT, st, 0, (double)B * N * (64 + 4) + arows * 4.0);
     HIP_TRY(launch_select(v_cache, v_prev, B, N, w_a, w_v, quota, act, s->idx, s->pos,
-                          s->record_scores ? s->score : nullptr, st));
+                          s->record_scores ? s->score : nullptr, s->sel_ws, st));
     idx = s->idx;
     pos = s->pos;
   }
@@ -569,6 +570,7 @@ int f3c_state_bytes_ex(const f3c_model* m, int32_t batch, uint32_t flags, size_t
   t += align256(A * m->dm * es);               // mlp hidden
   t += align256(A * 32);                       // v_act
   t += 3 * align256(R * 4);                    // idx, pos, score
+  t += align256(select_workspace_bytes(batch, m->N));   // selection workspace
   t += align256((size_t)m->L * 6 * d * 4);     // mod
   t += align256(2 * d * 4);                    // temb scratch
   t += align256((size_t)P * batch * m->Nc * m->dc * es);            // condition tokens
@@ -611,6 +613,7 @@ int f3c_state_create_ex(f3c_model* m, int32_t batch, uint32_t flags, void* state
   s->idx = (int32_t*)take(R * 4);
   s->pos = (int32_t*)take(R * 4);
   s->score = (float*)take(R * 4);
+  s->sel_ws = take(select_workspace_bytes(batch, m->N));
   s->mod = (float*)take((size_t)m->L * 6 * d * 4);
   s->temb = (float*)take(2 * d * 4);
   s->cond_t = take(P * batch * m->Nc * m->dc * es);
@@ -895,22 +898,47 @@ int f3c_profile_reset(f3c_state* s) {
 
 // ------------------------------------------------------------ operator entries
 
-int f3c_op_select(int32_t batch, int32_t n_tokens, const float* v_cache, const float* v_prev, float omega,
-                  const int32_t* n_cache_host, int32_t* idx_active, int32_t* pos, float* score, f3c_stream stream) {
+int f3c_op_select_workspace_bytes(int32_t batch, int32_t n_tokens, size_t* bytes) {
+  if (!bytes) return fail(F3C_EINVAL, "NULL argument");
+  if (batch < 1 || batch > F3C_MAX_BATCH) return fail(F3C_EINVAL, "batch must be in 1..%d", F3C_MAX_BATCH);
+  if (n_tokens < 1 || n_tokens > F3C_MAX_TOKENS) return fail(F3C_EINVAL, "n_tokens must be in 1..%d", F3C_MAX_TOKENS);
+  *bytes = select_workspace_bytes(batch, n_tokens);
+  return F3C_OK;
+}
+
+namespace {
+
+int select_args(int32_t batch, int32_t n_tokens, const float* v_cache, const float* v_prev, float omega,
+                const int32_t* n_cache_host, int32_t* idx_active, int32_t* pos, Segs* quota, Segs* act) {
   if (batch < 1 || batch > F3C_MAX_BATCH) return fail(F3C_EINVAL, "batch must be in 1..%d", F3C_MAX_BATCH);
   if (n_tokens < 1 || n_tokens > F3C_MAX_TOKENS) return fail(F3C_EINVAL, "n_tokens must be in 1..%d", F3C_MAX_TOKENS);
   if (!v_cache || !v_prev || !n_cache_host || !idx_active || !pos) return fail(F3C_EINVAL, "NULL argument");
   if (!(omega >= 0.0f && omega <= 1.0f)) return fail(F3C_EINVAL, "omega must be in [0, 1]");
-  Segs quota{}, act{};
-  quota.B = act.B = batch;
+  *quota = Segs{};
+  *act = Segs{};
+  quota->B = act->B = batch;
   for (int b = 0; b < batch; ++b) {
     const int c = n_cache_host[b];
     if (c < 0 || c > n_tokens) return fail(F3C_EINVAL, "n_cache[%d] = %d outside [0, %d]", b, c, n_tokens);
-    quota.off[b] = c;
-    act.off[b + 1] = act.off[b] + n_tokens - c;
+    quota->off[b] = c;
+    act->off[b + 1] = act->off[b] + n_tokens - c;
   }
+  return F3C_OK;
+}
+
+}  // namespace
+
+int f3c_op_select(int32_t batch, int32_t n_tokens, const float* v_cache, const float* v_prev, float omega,
+                  const int32_t* n_cache_host, int32_t* idx_active, int32_t* pos, float* score, void* workspace,
+                  size_t workspace_bytes, f3c_stream stream) {
+  Segs quota, act;
+  if (int rc = select_args(batch, n_tokens, v_cache, v_prev, omega, n_cache_host, idx_active, pos, &quota, &act))
+    return rc;
+  if (!workspace || ((uintptr_t)workspace & 255)) return fail(F3C_EINVAL, "workspace must be a 256-byte aligned buffer");
+  const size_t need = select_workspace_bytes(batch, n_tokens);
+  if (workspace_bytes < need) return fail(F3C_ENOMEM, "workspace %zu < %zu bytes", workspace_bytes, need);
   HIP_TRY(launch_select(v_cache, v_prev, batch, n_tokens, omega, 1.0f - omega, quota, act, idx_active, pos, score,
-                        (hipStream_t)stream));
+                        workspace, (hipStream_t)stream));
   return F3C_OK;
 }
 

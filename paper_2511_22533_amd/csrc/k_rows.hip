@@ -48,6 +48,85 @@ __global__ __launch_bounds__(256) void k_embed(const float* __restrict__ x, int 
   }
 }
 
+// The same for bf16 models with d a multiple of 256, streaming rows. A row is
+// split over WPR waves (WPR divides G = d / 256, the column groups of 256);
+// lane l of a wave owns columns 256 g + 4 l .. +3 of its GPW = G / WPR groups
+// and keeps their input weights (packed bf16) and biases in registers, so a
+// row costs only its 32-byte x row (one address per wave), its bf16 position
+// row (8-byte loads) and its f32 output row (16-byte stores). Wave w handles
+// part w % WPR of rows w / WPR + k * walkers, U rows per round; the token
+// indices of the next round are loaded while the current round's rows are
+// fetched, so each round waits for one memory round trip. Same operation
+// order as k_embed.
+template <int G, int WPR, int U = 8>
+__global__ __launch_bounds__(256) void k_embed_rows(const float* __restrict__ x, int N, const int32_t* __restrict__ idx,
+                                                    Segs act, const bf16* __restrict__ w_in,
+                                                    const float* __restrict__ b_in, const bf16* __restrict__ ptab,
+                                                    float* __restrict__ h, int64_t dup) {
+  constexpr int D = G * 256;
+  constexpr int GPW = G / WPR;
+  const int lane = threadIdx.x & 63;
+  const int gw = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int part = gw % WPR;
+  const int walkers = gridDim.x * 4 / WPR;       // waves per part
+  const int total = act.off[act.B];
+  const int first = gw / WPR;
+  // token of row r (idx may be null: identity within the segment), and its sample
+  auto token = [&](int r, int& b) {
+    b = find_segment(act.off, act.B, r);
+    return idx ? idx[r] : r - act.off[b];
+  };
+  int nb[U], ni[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) ni[u] = token(min(first + u * walkers, total - 1), nb[u]);
+  bf16x8 w[GPW][4];
+  float4 bias[GPW];
+#pragma unroll
+  for (int g = 0; g < GPW; ++g) {
+    const int n0 = 256 * (part * GPW + g) + 4 * lane;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[g][e] = *reinterpret_cast<const bf16x8*>(w_in + (size_t)(n0 + e) * 8);
+    bias[g] = *reinterpret_cast<const float4*>(b_in + n0);
+  }
+  for (int r0 = first; r0 < total; r0 += U * walkers) {
+    float xv[U][8];
+    bf16x4 pv[U][GPW];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {     // rows past the end repeat the last one (loads only)
+      const float4* xr = reinterpret_cast<const float4*>(x + ((size_t)nb[u] * N + ni[u]) * 8);
+      const float4 x0 = xr[0], x1 = xr[1];
+      xv[u][0] = x0.x; xv[u][1] = x0.y; xv[u][2] = x0.z; xv[u][3] = x0.w;
+      xv[u][4] = x1.x; xv[u][5] = x1.y; xv[u][6] = x1.z; xv[u][7] = x1.w;
+#pragma unroll
+      for (int g = 0; g < GPW; ++g)
+        pv[u][g] = *reinterpret_cast<const bf16x4*>(ptab + (size_t)ni[u] * D + 256 * (part * GPW + g) + 4 * lane);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) ni[u] = token(min(r0 + (U + u) * walkers, total - 1), nb[u]);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int row = r0 + u * walkers;
+      if (row >= total) break;
+      float* hr = h + (size_t)row * D;
+#pragma unroll
+      for (int g = 0; g < GPW; ++g) {
+        float o[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float acc = 0.0f;
+#pragma unroll
+          for (int c = 0; c < 8; ++c) acc += xv[u][c] * static_cast<float>(w[g][e][c]);
+          o[e] = acc + (&bias[g].x)[e] + static_cast<float>(pv[u][g][e]);
+        }
+        const float4 v = make_float4(o[0], o[1], o[2], o[3]);
+        const int col = 256 * (part * GPW + g) + 4 * lane;
+        *reinterpret_cast<float4*>(hr + col) = v;
+        if (dup) *reinterpret_cast<float4*>(hr + dup * D + col) = v;
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------------- LayerNorm (+mod)
 template <int NPL>
 __device__ __forceinline__ void row_stats(const float (&v)[NPL], float& mean, float& rstd) {
@@ -416,6 +495,22 @@ hipError_t launch_embed(int dt, const float* x, int N, const int32_t* idx, const
   const int rows = act.off[act.B];
   if (rows == 0) return hipSuccess;
   dim3 grid((rows + 3) / 4);
+  if (dt == DT_BF16 && d % 256 == 0 && d <= 2048) {
+    // streaming rows, 8 per round; at most 768 workgroups (three per CU at
+    // this kernel's register use, so that all are resident in one round)
+    const int wpr = std::min(d / 256, 4);
+    const int wgs = std::max(1, std::min((rows * wpr + 31) / 32, 768));
+    const bf16* w = (const bf16*)w_in;
+    const bf16* p = (const bf16*)pos_table;
+    switch (d / 256) {
+      case 1: launch(k_embed_rows<1, 1>, dim3(wgs), dim3(256), 0, s, x, N, idx, act, w, b_in, p, h, dup); break;
+      case 2: launch(k_embed_rows<2, 2>, dim3(wgs), dim3(256), 0, s, x, N, idx, act, w, b_in, p, h, dup); break;
+      case 4: launch(k_embed_rows<4, 4>, dim3(wgs), dim3(256), 0, s, x, N, idx, act, w, b_in, p, h, dup); break;
+      case 8: launch(k_embed_rows<8, 4>, dim3(wgs), dim3(256), 0, s, x, N, idx, act, w, b_in, p, h, dup); break;
+      default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
   if (dt == DT_BF16)
     F3C_NPL_LAUNCH(d, k_embed, bf16, grid, s, x, N, idx, act, (const bf16*)w_in, b_in, (const bf16*)pos_table, h,
                    dup);

@@ -1,15 +1,20 @@
 // Spatiotemporal Stability Criterion scoring and lowest-score selection
-// (Sec. 4.2, Eqs. 2, 6, 7; Algorithm 1, SSC), one 1024-thread workgroup per
-// sample.
+// (Sec. 4.2, Eqs. 2, 6, 7; Algorithm 1, SSC) in two kernels.
 //
-// Phase 1 computes V_i = ||v_cache_i|| and A_i = ||v_cache_i - v_prev_i|| with
-// a sequential float32 sum of squares (no fused multiply-add, correctly rounded
-// sqrt) and reduces their per-sample min/max. Phase 2 forms the score
-// C_i = w_a * norm(A_i) + w_v * norm(V_i) and an order-preserving 32-bit key
-// (NaN -> largest). Phase 3 finds the key of rank c-1 by an exact 4 x 8-bit
-// radix select over the keys held in LDS. Phase 4 scans the keys in token
-// order: a token is cached if its key is smaller, or equal and among the first
-// r equal keys, which reproduces a stable ascending sort truncated at c.
+// k_score_stats streams the two velocity caches over the whole chip (one
+// 256-thread workgroup per 1024 tokens of a sample): V_i = ||v_cache_i|| and
+// A_i = ||v_cache_i - v_prev_i|| with a sequential float32 sum of squares (no
+// fused multiply-add, correctly rounded sqrt), written as (V_i, A_i) pairs,
+// and each workgroup's min/max of both. min/max are exact and order-free
+// (the magnitudes are never -0; NaN is ignored), so the per-sample extremes do
+// not depend on how the tokens are split.
+//
+// k_select runs one 1024-thread workgroup per sample: it reduces the partial
+// extremes, forms the score C_i = w_a * norm(A_i) + w_v * norm(V_i) and an
+// order-preserving 32-bit key (NaN -> largest) per token into LDS, finds the
+// key of rank c-1 by an exact 4 x 8-bit radix select, and scans the keys in
+// token order: a token is cached if its key is smaller, or equal and among the
+// first r equal keys, which reproduces a stable ascending sort truncated at c.
 #include "common.h"
 #include "kernels.h"
 
@@ -19,8 +24,12 @@ namespace f3c {
 
 namespace {
 
-constexpr int kThreads = 1024;
-constexpr int kPer = kMaxTokens / kThreads;   // tokens per thread in phase 1
+constexpr int kThreads = 1024;       // select: one workgroup per sample
+constexpr int kStatThreads = 256;    // score statistics: tokens streamed over the chip
+constexpr int kStatPer = 4;
+constexpr int kChunk = kStatThreads * kStatPer;
+constexpr int kMaxChunks = kMaxTokens / kChunk;
+static_assert(kMaxChunks <= 64, "the select kernel reduces the partial extremes in one wave");
 
 __device__ __forceinline__ float sumsq8(const float4& a, const float4& b) {
   float s = 0.0f;
@@ -57,77 +66,68 @@ __device__ __forceinline__ float norm_term(float a, float lo, float hi) {
   return div_rn(__fsub_rn(a, lo), __fsub_rn(hi, lo));
 }
 
-// Exclusive block scan of one int per thread; returns the exclusive prefix and
-// the block total. Uses the 16-entry scratch `ws`.
-__device__ int block_exclusive_scan(int v, int* ws, int* total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int x = v;
+// In-place exclusive prefix sum of v[0..n) (n <= 512) by wave 0: lane l
+// sums entries 8l .. 8l+7, the lanes scan their totals, then each lane
+// writes its entries' exclusive prefixes. Callers place barriers around it.
+__device__ void segment_exclusive_scan(int* v, int n, int lane, int wave) {
+  if (wave != 0) return;
+  int loc[8];
+  int sum = 0;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int k = 8 * lane + e;
+    loc[e] = k < n ? v[k] : 0;
+    sum += loc[e];
+  }
+  int x = sum;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
-    int y = __shfl_up(x, o);
+    const int y = __shfl_up(x, o);
     if (lane >= o) x += y;
   }
-  if (lane == 63) ws[wave] = x;
-  __syncthreads();
-  if (wave == 0) {
-    int w = lane < kThreads / 64 ? ws[lane] : 0;
+  int run = x - sum;
 #pragma unroll
-    for (int o = 1; o < 16; o <<= 1) {
-      int y = __shfl_up(w, o);
-      if (lane >= o) w += y;
-    }
-    if (lane < kThreads / 64) ws[lane] = w;
+  for (int e = 0; e < 8; ++e) {
+    const int k = 8 * lane + e;
+    if (k < n) v[k] = run;
+    run += loc[e];
   }
-  __syncthreads();
-  int before = (wave > 0 ? ws[wave - 1] : 0) + x - v;
-  *total = ws[kThreads / 64 - 1];
-  __syncthreads();
-  return before;
 }
 
-__global__ __launch_bounds__(kThreads) void k_score_select(const float* __restrict__ v_cache,
-                                                           const float* __restrict__ v_prev, int N, float w_a,
-                                                           float w_v, Segs n_cache, Segs act,
-                                                           int32_t* __restrict__ idx_active,
-                                                           int32_t* __restrict__ pos, float* __restrict__ score) {
-  __shared__ uint32_t keys[kMaxTokens];
-  __shared__ float red[4][kThreads / 64];
-  __shared__ int hist[256];
-  __shared__ int scan_ws[kThreads / 64];
-  __shared__ int sel[2];
-
-  const int b = blockIdx.x;
+// (V_i, A_i) of every token of the samples with c_b > 0, and each
+// workgroup's extremes (loV, hiV, loA, hiA) at partial[b * chunks + chunk].
+__global__ __launch_bounds__(kStatThreads) void k_score_stats(const float* __restrict__ v_cache,
+                                                             const float* __restrict__ v_prev, int N, Segs n_cache,
+                                                             float2* __restrict__ va, float4* __restrict__ partial,
+                                                             int chunks) {
+  __shared__ float4 red[kStatThreads / 64];
+  const int b = blockIdx.y, chunk = blockIdx.x;
+  if (n_cache.off[b] == 0) return;
   const int tid = threadIdx.x;
-  const int c = n_cache.off[b];
-  const int row0 = act.off[b];
   const size_t base = (size_t)b * N;
-
-  if (c == 0) {  // full step for this sample: identity selection, no scoring
-    for (int i = tid; i < N; i += kThreads) {
-      idx_active[row0 + i] = i;
-      pos[base + i] = row0 + i;
-    }
-    return;
+  float4 c0[kStatPer], c1[kStatPer], p0[kStatPer], p1[kStatPer];
+#pragma unroll
+  for (int j = 0; j < kStatPer; ++j) {
+    const int i = min(chunk * kChunk + j * kStatThreads + tid, N - 1);   // clamped: loads stay in bounds
+    const float4* pc = reinterpret_cast<const float4*>(v_cache + (base + i) * 8);
+    const float4* pp = reinterpret_cast<const float4*>(v_prev + (base + i) * 8);
+    c0[j] = pc[0];
+    c1[j] = pc[1];
+    p0[j] = pp[0];
+    p1[j] = pp[1];
   }
-
-  // Phase 1: magnitudes and per-sample extremes (NaN ignored by fminf/fmaxf).
-  float V[kPer], A[kPer];
   float loV = INFINITY, hiV = -INFINITY, loA = INFINITY, hiA = -INFINITY;
 #pragma unroll
-  for (int j = 0; j < kPer; ++j) {
-    const int i = tid + j * kThreads;
-    V[j] = 0.0f;
-    A[j] = 0.0f;
+  for (int j = 0; j < kStatPer; ++j) {
+    const int i = chunk * kChunk + j * kStatThreads + tid;
     if (i < N) {
-      const float4* pc = reinterpret_cast<const float4*>(v_cache + (base + i) * 8);
-      const float4* pp = reinterpret_cast<const float4*>(v_prev + (base + i) * 8);
-      float4 c0 = pc[0], c1 = pc[1], p0 = pp[0], p1 = pp[1];
-      V[j] = sqrt_rn(sumsq8(c0, c1));
-      A[j] = sqrt_rn(sumsq8(sub4(c0, p0), sub4(c1, p1)));
-      loV = fminf(loV, V[j]);
-      hiV = fmaxf(hiV, V[j]);
-      loA = fminf(loA, A[j]);
-      hiA = fmaxf(hiA, A[j]);
+      const float V = sqrt_rn(sumsq8(c0[j], c1[j]));
+      const float A = sqrt_rn(sumsq8(sub4(c0[j], p0[j]), sub4(c1[j], p1[j])));
+      va[base + i] = make_float2(V, A);
+      loV = fminf(loV, V);
+      hiV = fmaxf(hiV, V);
+      loA = fminf(loA, A);
+      hiA = fmaxf(hiA, A);
     }
   }
 #pragma unroll
@@ -137,47 +137,97 @@ __global__ __launch_bounds__(kThreads) void k_score_select(const float* __restri
     loA = fminf(loA, __shfl_xor(loA, o));
     hiA = fmaxf(hiA, __shfl_xor(hiA, o));
   }
-  const int lane = tid & 63, wave = tid >> 6;
-  if (lane == 0) {
-    red[0][wave] = loV;
-    red[1][wave] = hiV;
-    red[2][wave] = loA;
-    red[3][wave] = hiA;
-  }
+  if ((tid & 63) == 0) red[tid >> 6] = make_float4(loV, hiV, loA, hiA);
   __syncthreads();
-  loV = red[0][0];
-  hiV = red[1][0];
-  loA = red[2][0];
-  hiA = red[3][0];
-  for (int w = 1; w < kThreads / 64; ++w) {
-    loV = fminf(loV, red[0][w]);
-    hiV = fmaxf(hiV, red[1][w]);
-    loA = fminf(loA, red[2][w]);
-    hiA = fmaxf(hiA, red[3][w]);
-  }
-
-  // Phase 2: scores and order keys.
+  if (tid == 0) {
+    float4 m = red[0];
 #pragma unroll
-  for (int j = 0; j < kPer; ++j) {
-    const int i = tid + j * kThreads;
-    if (i < N) {
-      const float cs = __fadd_rn(__fmul_rn(w_a, norm_term(A[j], loA, hiA)),
-                                 __fmul_rn(w_v, norm_term(V[j], loV, hiV)));
-      keys[i] = order_key(cs);
-      if (score) score[base + i] = cs;
+    for (int w = 1; w < kStatThreads / 64; ++w) {
+      m.x = fminf(m.x, red[w].x);
+      m.y = fmaxf(m.y, red[w].y);
+      m.z = fminf(m.z, red[w].z);
+      m.w = fmaxf(m.w, red[w].w);
     }
+    partial[(size_t)b * chunks + chunk] = m;
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void k_select(const float2* __restrict__ va, const float4* __restrict__ partial,
+                                                     int chunks, int N, float w_a, float w_v, Segs n_cache, Segs act,
+                                                     int32_t* __restrict__ idx_active, int32_t* __restrict__ pos,
+                                                     float* __restrict__ score) {
+  __shared__ uint32_t keys[kMaxTokens];
+  __shared__ int hist[256];
+  __shared__ int cnt_eq[kMaxTokens / 64], cnt_act[kMaxTokens / 64];   // per (round, wave)
+  __shared__ int sel[2];
+  __shared__ float4 ext;
+
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int c = n_cache.off[b];
+  const int row0 = act.off[b];
+  const size_t base = (size_t)b * N;
+  const int lane = tid & 63, wave = tid >> 6;
+
+  if (c == 0) {  // full step for this sample: identity selection, no scoring
+    for (int i = tid; i < N; i += kThreads) {
+      idx_active[row0 + i] = i;
+      pos[base + i] = row0 + i;
+    }
+    return;
+  }
+
+  // The sample's extremes from the partials (chunks <= 64: one wave).
+  if (wave == 0) {
+    float4 m = lane < chunks ? partial[(size_t)b * chunks + lane] : make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      m.x = fminf(m.x, __shfl_xor(m.x, o));
+      m.y = fmaxf(m.y, __shfl_xor(m.y, o));
+      m.z = fminf(m.z, __shfl_xor(m.z, o));
+      m.w = fmaxf(m.w, __shfl_xor(m.w, o));
+    }
+    if (lane == 0) ext = m;
+  }
+  __syncthreads();
+  const float loV = ext.x, hiV = ext.y, loA = ext.z, hiA = ext.w;
+
+  // Scores and order keys.
+  for (int i = tid; i < N; i += kThreads) {
+    const float2 p = va[base + i];
+    const float cs = __fadd_rn(__fmul_rn(w_a, norm_term(p.y, loA, hiA)), __fmul_rn(w_v, norm_term(p.x, loV, hiV)));
+    keys[i] = order_key(cs);
+    if (score) score[base + i] = cs;
   }
   __syncthreads();
 
-  // Phase 3: radix select of the key with 0-based rank c-1.
+  // Radix select of the key with 0-based rank c-1. The keys of one sample
+  // mostly share their leading byte (scores lie in [0, 1]), so a wave first
+  // merges the lanes that share the bin of its lowest pending lane, twice,
+  // with one LDS atomic per merged bin (same-address atomics of one
+  // instruction would serialise); the lanes left add their own key.
+  const uint64_t below = (1ull << lane) - 1ull;   // lanes before this one
   uint32_t prefix = 0, mask = 0;
   int r = c;
   for (int shift = 24; shift >= 0; shift -= 8) {
     for (int i = tid; i < 256; i += kThreads) hist[i] = 0;
     __syncthreads();
-    for (int i = tid; i < N; i += kThreads) {
-      const uint32_t k = keys[i];
-      if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1);
+    for (int i0 = 0; i0 < N; i0 += kThreads) {     // whole waves iterate together (ballots below)
+      const int i = i0 + tid;
+      const uint32_t k = i < N ? keys[i] : 0u;
+      const bool in = i < N && (k & mask) == prefix;
+      const int bin = (int)((k >> shift) & 255u);
+      uint64_t todo = __ballot(in);
+#pragma unroll
+      for (int it = 0; it < 2; ++it) {
+        if (!todo) break;
+        const int leader = __ffsll((unsigned long long)todo) - 1;
+        const int lb = __shfl(bin, leader);
+        const uint64_t same = __ballot(in && bin == lb);
+        if (lane == leader) atomicAdd(&hist[lb], __popcll(same));
+        todo &= ~same;
+      }
+      if ((todo >> lane) & 1ull) atomicAdd(&hist[bin], 1);
     }
     __syncthreads();
     if (wave == 0) {
@@ -208,37 +258,47 @@ __global__ __launch_bounds__(kThreads) void k_score_select(const float* __restri
   }
   const uint32_t kstar = prefix;   // key of rank c-1; r = cached tokens among keys == kstar
 
-  // Phase 4: token-order scan. Thread t owns the contiguous range [t*P, t*P + P).
-  const int P = (N + kThreads - 1) / kThreads;
-  const int i0 = min(N, tid * P), i1 = min(N, i0 + P);
-  int eq_local = 0;
-  for (int i = i0; i < i1; ++i) eq_local += (keys[i] == kstar);
-  int tot;
-  int eq_before = block_exclusive_scan(eq_local, scan_ws, &tot);
-  int act_local = 0;
-  {
-    int e = eq_before;
-    for (int i = i0; i < i1; ++i) {
-      const uint32_t k = keys[i];
-      bool cached = k < kstar;
-      if (k == kstar) { cached = e < r; ++e; }
-      act_local += !cached;
-    }
+  // Token-order scan. Token i = 1024 j + 64 w + lane is handled by lane
+  // `lane` of wave w in round j, so (j, w, lane) runs in token order. A token
+  // is cached when its key is below kstar, or equal and among the first r
+  // equal keys. Per (round, wave) counts of equal keys, then of active
+  // tokens, go through an exclusive scan in LDS; a lane's rank inside its
+  // wave is the popcount of the ballot below it. Loads and stores of one
+  // wave touch 64 consecutive tokens.
+  const int rounds = (N + kThreads - 1) / kThreads;
+  const int nw = kThreads / 64;
+  for (int j = 0; j < rounds; ++j) {
+    const int i = j * kThreads + tid;
+    const uint64_t eq = __ballot(i < N && keys[i] == kstar);
+    if (lane == 0) cnt_eq[j * nw + wave] = __popcll(eq);
   }
-  int act_before = block_exclusive_scan(act_local, scan_ws, &tot);
-  {
-    int e = eq_before, a = row0 + act_before;
-    for (int i = i0; i < i1; ++i) {
-      const uint32_t k = keys[i];
-      bool cached = k < kstar;
-      if (k == kstar) { cached = e < r; ++e; }
-      if (cached) {
-        pos[base + i] = -1;
-      } else {
-        pos[base + i] = a;
-        idx_active[a] = i;
-        ++a;
-      }
+  __syncthreads();
+  segment_exclusive_scan(cnt_eq, rounds * nw, lane, wave);
+  __syncthreads();
+  for (int j = 0; j < rounds; ++j) {
+    const int i = j * kThreads + tid;
+    const uint32_t k = i < N ? keys[i] : 0xFFFFFFFFu;
+    const bool is_eq = i < N && k == kstar;
+    const uint64_t eq = __ballot(is_eq);
+    const bool cached = k < kstar || (is_eq && cnt_eq[j * nw + wave] + __popcll(eq & below) < r);
+    const uint64_t act_mask = __ballot(i < N && !cached);
+    if (lane == 0) cnt_act[j * nw + wave] = __popcll(act_mask);
+  }
+  __syncthreads();
+  segment_exclusive_scan(cnt_act, rounds * nw, lane, wave);
+  __syncthreads();
+  for (int j = 0; j < rounds; ++j) {
+    const int i = j * kThreads + tid;
+    const uint32_t k = i < N ? keys[i] : 0xFFFFFFFFu;
+    const bool is_eq = i < N && k == kstar;
+    const uint64_t eq = __ballot(is_eq);
+    const bool cached = k < kstar || (is_eq && cnt_eq[j * nw + wave] + __popcll(eq & below) < r);
+    const bool active = i < N && !cached;
+    const uint64_t act_mask = __ballot(active);
+    if (i < N) {
+      const int a = row0 + cnt_act[j * nw + wave] + __popcll(act_mask & below);
+      pos[base + i] = active ? a : -1;
+      if (active) idx_active[a] = i;
     }
   }
 }
@@ -273,11 +333,21 @@ hipError_t launch_force_active(const int32_t* idx_in, const Segs& act, int N, in
   return hipGetLastError();
 }
 
+size_t select_workspace_bytes(int B, int N) {
+  const int chunks = (N + kChunk - 1) / kChunk;
+  return (((size_t)B * N * sizeof(float2) + 255) & ~(size_t)255) + (size_t)B * chunks * sizeof(float4);
+}
+
 hipError_t launch_select(const float* v_cache, const float* v_prev, int B, int N, float w_a, float w_v,
                          const Segs& n_cache, const Segs& act, int32_t* idx_active, int32_t* pos,
-                         float* score, hipStream_t s) {
-  launch(k_score_select, dim3(B), dim3(kThreads), 0, s, v_cache, v_prev, N, w_a, w_v, n_cache, act,
-                     idx_active, pos, score);
+                         float* score, void* workspace, hipStream_t s) {
+  const int chunks = (N + kChunk - 1) / kChunk;
+  float2* va = static_cast<float2*>(workspace);
+  float4* partial = reinterpret_cast<float4*>(static_cast<char*>(workspace) +
+                                              (((size_t)B * N * sizeof(float2) + 255) & ~(size_t)255));
+  launch(k_score_stats, dim3(chunks, B), dim3(kStatThreads), 0, s, v_cache, v_prev, N, n_cache, va, partial, chunks);
+  launch(k_select, dim3(B), dim3(kThreads), 0, s, (const float2*)va, (const float4*)partial, chunks, N, w_a, w_v,
+         n_cache, act, idx_active, pos, score);
   return hipGetLastError();
 }
 

@@ -8,7 +8,7 @@
 namespace f3c {
 
 constexpr int kMaxBatch = 64;          // samples per step (segment tables travel by value)
-constexpr int kMaxTokens = 32768;      // tokens per sample handled by the one-workgroup selector
+constexpr int kMaxTokens = 32768;      // tokens per sample (the selector keeps one sample's keys in LDS)
 
 // Segment table passed by value: sample b owns rows [off[b], off[b+1]).
 struct Segs {
@@ -23,14 +23,18 @@ enum Epilogue { EPI_STORE = 0, EPI_GELU = 1, EPI_RESID = 2 };
 // kernel trace attributes time to the projection / attention it belongs to.
 enum Site { SITE_OP = 0, SITE_QKV, SITE_O, SITE_Q, SITE_CO, SITE_FC1, SITE_FC2, SITE_COND, SITE_SELF, SITE_CROSS };
 
-// Stability score + lowest-score selection, one workgroup per sample.
-// v_cache, v_prev: f32 [B][N][8]. n_cache: per-sample cached counts (by value).
-// act: active-row offsets (by value). Writes idx_active[act.off[b] + r] (ascending
-// token index of the r-th active token), pos[b*N + i] (packed row or -1) and,
-// when score != nullptr, the float32 score of every token (only for c_b > 0).
+// Stability score + lowest-score selection: a streaming statistics pass over
+// all tokens, then one workgroup per sample. v_cache, v_prev: f32 [B][N][8].
+// n_cache: per-sample cached counts (by value). act: active-row offsets (by
+// value). Writes idx_active[act.off[b] + r] (ascending token index of the r-th
+// active token), pos[b*N + i] (packed row or -1) and, when score != nullptr,
+// the float32 score of every token (only for c_b > 0). workspace (256-byte
+// aligned, select_workspace_bytes(B, N) bytes) holds the per-token magnitude
+// pairs and the per-workgroup extremes between the two kernels.
+size_t select_workspace_bytes(int B, int N);
 hipError_t launch_select(const float* v_cache, const float* v_prev, int B, int N, float w_a, float w_v,
                          const Segs& n_cache, const Segs& act, int32_t* idx_active, int32_t* pos,
-                         float* score, hipStream_t s);
+                         float* score, void* workspace, hipStream_t s);
 
 // Teacher-forced selection: idx_out[r] = idx_in[r] (clamped into [0, N)) for
 // the act.off[B] listed rows, pos[b][i] = r for listed tokens, -1 elsewhere.

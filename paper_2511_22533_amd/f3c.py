@@ -79,7 +79,8 @@ _SIGS = {
     "f3c_profile_enable": (c_int, [c_p, ctypes.c_uint32]),
     "f3c_profile_read": (c_int, [c_p, c_int, ctypes.POINTER(c_i64), P_d, P_d, P_d]),
     "f3c_profile_reset": (c_int, [c_p]),
-    "f3c_op_select": (c_int, [c_int, c_int, c_p, c_p, c_f, P_i32, c_p, c_p, c_p, c_p]),
+    "f3c_op_select": (c_int, [c_int, c_int, c_p, c_p, c_f, P_i32, c_p, c_p, c_p, c_p, c_sz, c_p]),
+    "f3c_op_select_workspace_bytes": (c_int, [c_int, c_int, ctypes.POINTER(c_sz)]),
     "f3c_op_gemm": (c_int, [c_int, c_int, c_int, c_int, c_int, c_p, c_int, c_p, c_int, c_p, c_p, c_p, c_int, c_p,
                             c_int, c_p]),
     "f3c_op_attention": (c_int, [c_int, c_int, c_int, c_int, P_i32, P_i32, c_p, c_int, c_p, c_int, c_p, c_int, c_p,
@@ -422,10 +423,22 @@ class State:
 
 # ---------------------------------------------------------------- operator calls
 
-def op_select(v_cache, v_prev, omega: float, n_cache: Sequence[int], idx_active, pos, score=None, stream=None):
+def select_workspace_bytes(batch: int, n_tokens: int) -> int:
+    b = c_sz()
+    check(lib().f3c_op_select_workspace_bytes(batch, n_tokens, ctypes.byref(b)))
+    return b.value
+
+
+def op_select(v_cache, v_prev, omega: float, n_cache: Sequence[int], idx_active, pos, score=None, workspace=None,
+              stream=None):
+    """workspace: a device uint8 tensor of at least select_workspace_bytes(B, N) (allocated here if None)."""
+    import torch
     B, N = v_cache.shape[0], v_cache.shape[1]
+    if workspace is None:
+        workspace = torch.empty(select_workspace_bytes(B, N), dtype=torch.uint8, device=v_cache.device)
     check(lib().f3c_op_select(B, N, v_cache.data_ptr(), v_prev.data_ptr(), omega, _i32(n_cache),
-                              idx_active.data_ptr(), pos.data_ptr(), _ptr(score), _stream(stream)))
+                              idx_active.data_ptr(), pos.data_ptr(), _ptr(score), workspace.data_ptr(),
+                              workspace.numel() * workspace.element_size(), _stream(stream)))
 
 
 def op_gemm(dtype: int, epilogue: int, A, W, bias, out=None, resid=None, gate=None, stream=None):

@@ -128,10 +128,16 @@ def test_steps_need_loaded_weights_and_valid_quota(L):
 
 def test_op_entry_validation_is_host_side(L):
     q = f3c._i32([0, 5])
-    assert L.f3c_op_select(0, 512, 1, 1, 0.7, q, 1, 1, None, None) == f3c.F3C_EINVAL
-    assert L.f3c_op_select(1, 512, 1, 1, 1.5, q, 1, 1, None, None) == f3c.F3C_EINVAL
-    assert L.f3c_op_select(1, 4, 1, 1, 0.7, f3c._i32([5]), 1, 1, None, None) == f3c.F3C_EINVAL
-    assert L.f3c_op_select(1, 40000, 1, 1, 0.7, f3c._i32([5]), 1, 1, None, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_select(0, 512, 1, 1, 0.7, q, 1, 1, None, 256, 1 << 20, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_select(1, 512, 1, 1, 1.5, q, 1, 1, None, 256, 1 << 20, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_select(1, 4, 1, 1, 0.7, f3c._i32([5]), 1, 1, None, 256, 1 << 20, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_select(1, 40000, 1, 1, 0.7, f3c._i32([5]), 1, 1, None, 256, 1 << 20, None) == f3c.F3C_EINVAL
+    # workspace: missing, misaligned, too small
+    assert L.f3c_op_select(1, 512, 1, 1, 0.7, q, 1, 1, None, None, 1 << 20, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_select(1, 512, 1, 1, 0.7, q, 1, 1, None, 128, 1 << 20, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_select(1, 512, 1, 1, 0.7, q, 1, 1, None, 256, 64, None) == f3c.F3C_ENOMEM
+    assert f3c.select_workspace_bytes(1, 512) == 512 * 8 + 16
+    assert f3c.select_workspace_bytes(4, 32768) == 4 * 32768 * 8 + 4 * 32 * 16
     assert L.f3c_op_gemm(1, 0, 16, 100, 64, 1, 64, 1, 64, 1, None, 1, 100, None, 0, None) == f3c.F3C_EINVAL
     assert L.f3c_op_gemm(1, 0, 16, 128, 40, 1, 40, 1, 40, 1, None, 1, 128, None, 0, None) == f3c.F3C_EINVAL
     assert L.f3c_op_gemm(1, 0, 16, 128, 64, 1, 64, 1, 64, 1, None, 1, 130, None, 0, None) == f3c.F3C_EINVAL

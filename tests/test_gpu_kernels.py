@@ -59,7 +59,7 @@ def _check_select(torch, vc, vp, n_cache, omega=0.7):
         row += n
 
 
-@pytest.mark.parametrize("B,N", [(1, 512), (1, 4096), (4, 4096), (1, 32768), (3, 1000), (2, 1)])
+@pytest.mark.parametrize("B,N", [(1, 512), (1, 4096), (4, 4096), (1, 32768), (3, 1000), (2, 1), (5, 3000), (16, 32768)])
 def test_select_bit_exact_random(torch, B, N):
     rng = np.random.default_rng(N + B)
     vc = rng.standard_normal((B, N, 8)).astype(np.float32)
