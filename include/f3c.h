@@ -308,6 +308,23 @@ int f3c_op_select(int32_t batch, int32_t n_tokens, const float* v_cache, const f
                   const int32_t* n_cache_host, int32_t* idx_active, int32_t* pos, float* score, void* workspace,
                   size_t workspace_bytes, f3c_stream stream);
 
+/* f3c_op_select without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation): the scratch lives in a fixed array in the library's
+ * device code, 4 MiB + 16 KiB on each GPU, held until the process ends. It
+ * serves at most F3C_NOALLOC_MAX_TOKENS tokens in all (batch * n_tokens);
+ * larger calls fail with F3C_EINVAL before enqueuing anything. Nothing in it
+ * needs clearing: a call overwrites what it reads. All calls on one GPU share
+ * the array, so calls that overlap in time on one GPU (different streams, or
+ * threads) race and must be ordered by the caller. Same arguments, results
+ * and errors as f3c_op_select otherwise; the results are bit-identical to
+ * it. No allocation, free or allocating library routine is called (the
+ * array's address is looked up once per device with hipGetSymbolAddress). */
+#define F3C_NOALLOC_MAX_TOKENS 524288
+int f3c_op_select_noalloc(int32_t batch, int32_t n_tokens, const float* v_cache, const float* v_prev, float omega,
+                          const int32_t* n_cache_host, int32_t* idx_active, int32_t* pos, float* score,
+                          f3c_stream stream);
+
 /* out/resid = A W^T + bias (+ epilogue). A: T [M][lda], W: T [N][ldw], bias f32 [N].
  * epilogue 0: out T [M][ldo] = value; 1: out = GELU_tanh(value);
  * 2: resid f32 [M][ldr] += (gate ? gate[n] : 1) * value.

@@ -942,6 +942,25 @@ int f3c_op_select(int32_t batch, int32_t n_tokens, const float* v_cache, const f
   return F3C_OK;
 }
 
+int f3c_op_select_noalloc(int32_t batch, int32_t n_tokens, const float* v_cache, const float* v_prev, float omega,
+                          const int32_t* n_cache_host, int32_t* idx_active, int32_t* pos, float* score,
+                          f3c_stream stream) {
+  Segs quota, act;
+  if (int rc = select_args(batch, n_tokens, v_cache, v_prev, omega, n_cache_host, idx_active, pos, &quota, &act))
+    return rc;
+  if ((int64_t)batch * n_tokens > F3C_NOALLOC_MAX_TOKENS)
+    return fail(F3C_EINVAL, "batch %d x %d tokens exceeds the static scratch's %d tokens", batch, n_tokens,
+                F3C_NOALLOC_MAX_TOKENS);
+  void* scratch = nullptr;
+  size_t have = 0;
+  HIP_TRY(select_static_scratch(&scratch, &have));
+  const size_t need = select_workspace_bytes(batch, n_tokens);
+  if (need > have) return fail(F3C_EINVAL, "selection scratch %zu > static %zu bytes", need, have);
+  HIP_TRY(launch_select(v_cache, v_prev, batch, n_tokens, omega, 1.0f - omega, quota, act, idx_active, pos, score,
+                        scratch, (hipStream_t)stream));
+  return F3C_OK;
+}
+
 int f3c_op_gemm(int32_t dtype, int32_t epilogue, int32_t M, int32_t N, int32_t K, const void* A, int32_t lda,
                 const void* W, int32_t ldw, const float* bias, const float* gate, void* out, int32_t ldo,
                 float* resid, int32_t ldr, f3c_stream stream) {

@@ -15,6 +15,9 @@
 // key of rank c-1 by an exact 4 x 8-bit radix select, and scans the keys in
 // token order: a token is cached if its key is smaller, or equal and among the
 // first r equal keys, which reproduces a stable ascending sort truncated at c.
+#include <mutex>
+#include <vector>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -331,6 +334,32 @@ hipError_t launch_force_active(const int32_t* idx_in, const Segs& act, int N, in
   const int rows = act.off[act.B];
   if (rows > 0) launch(k_force_scatter, dim3((unsigned)((rows + 255) / 256)), dim3(256), 0, s, idx_in, act, N, idx_out, pos);
   return hipGetLastError();
+}
+
+// Static selection scratch for callers that cannot allocate (the no-alloc
+// operator entry). Each device holds its own copy; its device address is
+// looked up once per device and kept, since host code must never pass the
+// symbol itself to a kernel.
+constexpr size_t kStaticScratchBytes = (size_t(4) << 20) + (size_t(16) << 10);
+static __device__ __align__(256) char scratch[kStaticScratchBytes];
+
+hipError_t select_static_scratch(void** ptr, size_t* bytes) {
+  static std::mutex mu;
+  static std::vector<void*> by_device;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(mu);
+  if ((int)by_device.size() <= dev) by_device.resize(dev + 1, nullptr);
+  if (!by_device[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    by_device[dev] = p;
+  }
+  *ptr = by_device[dev];
+  *bytes = kStaticScratchBytes;
+  return hipSuccess;
 }
 
 size_t select_workspace_bytes(int B, int N) {
