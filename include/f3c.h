@@ -339,6 +339,11 @@ int f3c_op_gemm(int32_t dtype, int32_t epilogue, int32_t M, int32_t N, int32_t K
  * of q (T, row stride ldq), its keys/values rows k_off[b]..k_off[b+1] of k/v;
  * head h uses columns h*head_dim..; o (T) gets one row per query.
  * head_dim in {32, 64}; offsets are host arrays of B+1 non-decreasing ints.
+ * q_prescaled = 1 declares that q holds the queries already multiplied by
+ * log2(e) / sqrt(head_dim), the softmax scale in base-2 units (as the step's
+ * projections store them, rounded once); 0 for plain queries. The result is
+ * softmax(Q K^T / sqrt(head_dim)) V either way (Sec. 4.2: attention over the
+ * active tokens).
  * workspace (device, 16-byte aligned, may be NULL) lets launches with few
  * query tiles and long key ranges split the key range over workgroups (when
  * that shortens each wave's chain of key tiles by enough to repay the merge):
@@ -349,7 +354,7 @@ int f3c_op_gemm(int32_t dtype, int32_t epilogue, int32_t M, int32_t N, int32_t K
 int f3c_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int32_t batch, const int32_t* q_off_host,
                      const int32_t* k_off_host, const void* q, int32_t ldq, const void* k, int32_t ldk,
                      const void* v, int32_t ldv, void* o, int32_t ldo, float* workspace, size_t workspace_bytes,
-                     f3c_stream stream);
+                     int32_t q_prescaled, f3c_stream stream);
 
 /* out T [rows][d] = LN(h) * (1 + scale) + shift (no affine LN, eps 1e-6);
  * shift/scale f32 [d] or both NULL. d in {128, 256, 512, 1024, 2048}. */

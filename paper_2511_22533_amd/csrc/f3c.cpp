@@ -299,8 +299,9 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
       }
       {
         Scope sc(s, F3C_PROF_GEMM_QKV, st, 2.0 * rows * 3 * d * d, proj_bytes(3 * dd, dd, false));
+        // queries stored times the attention's base-2 softmax scale (one rounding)
         HIP_TRY(launch_gemm(SITE_QKV, dt, EPI_STORE, rows, 3 * d, d, s->u, d, m->w(bw.qkv_w), d, m->b(bw.qkv_b),
-                            nullptr, s->qkv, 3 * d, nullptr, 0, st));
+                            nullptr, s->qkv, 3 * d, nullptr, 0, st, attention_q_scale(m->hd), d));
       }
       {
         double fl = 0;
@@ -309,7 +310,7 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
         Scope sc(s, F3C_PROF_ATTN_SELF, st, fl, 4.0 * r * dd * E);
         const char* q = static_cast<const char*>(s->qkv);
         HIP_TRY(launch_attention(SITE_SELF, dt, m->cfg.heads, m->hd, tact, tact, q, 3 * d, q + d * es, 3 * d,
-                                 q + 2 * d * es, 3 * d, s->att, d, s->ws, s->ws_bytes, st));
+                                 q + 2 * d * es, 3 * d, s->att, d, s->ws, s->ws_bytes, st, true));
       }
       {
         Scope sc(s, F3C_PROF_GEMM_O, st, 2.0 * rows * d * d, proj_bytes(dd, dd, true));
@@ -329,13 +330,13 @@ int run_step(f3c_state* s, float* x, double t, double t_next, const int32_t* n_c
       {
         Scope sc(s, F3C_PROF_GEMM_Q, st, 2.0 * rows * d * d, proj_bytes(dd, dd, false));
         HIP_TRY(launch_gemm(SITE_Q, dt, EPI_STORE, rows, d, d, s->u, d, m->w(bw.q_w), d, m->b(bw.q_b), nullptr,
-                            s->qc, d, nullptr, 0, st));
+                            s->qc, d, nullptr, 0, st, attention_q_scale(m->hd), d));
       }
       {
         Scope sc(s, F3C_PROF_ATTN_CROSS, st, 4.0 * rows * m->Nc * d, (2.0 * r + 2.0 * cond_rows) * dd * E);
         const char* kv = static_cast<const char*>(s->kv) + (size_t)l * 2 * d * es;
         HIP_TRY(launch_attention(SITE_CROSS, dt, m->cfg.heads, m->hd, tact, cond_segs, s->qc, d, kv, 2 * L * d,
-                                 kv + d * es, 2 * L * d, s->att, d, s->ws, s->ws_bytes, st));
+                                 kv + d * es, 2 * L * d, s->att, d, s->ws, s->ws_bytes, st, true));
       }
       {
         Scope sc(s, F3C_PROF_GEMM_CO, st, 2.0 * rows * d * d, proj_bytes(dd, dd, true));
@@ -982,9 +983,10 @@ int f3c_op_gemm(int32_t dtype, int32_t epilogue, int32_t M, int32_t N, int32_t K
 int f3c_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int32_t batch, const int32_t* q_off_host,
                      const int32_t* k_off_host, const void* q, int32_t ldq, const void* k, int32_t ldk,
                      const void* v, int32_t ldv, void* o, int32_t ldo, float* workspace, size_t workspace_bytes,
-                     f3c_stream stream) {
+                     int32_t q_prescaled, f3c_stream stream) {
   if (dtype != F3C_F32 && dtype != F3C_BF16) return fail(F3C_EINVAL, "bad dtype");
   if (head_dim != 32 && head_dim != 64) return fail(F3C_EINVAL, "head_dim must be 32 or 64");
+  if (q_prescaled != 0 && q_prescaled != 1) return fail(F3C_EINVAL, "q_prescaled must be 0 or 1");
   if (heads < 1 || heads > 65535) return fail(F3C_EINVAL, "bad heads");
   if (batch < 1 || batch > F3C_MAX_BATCH) return fail(F3C_EINVAL, "batch must be in 1..%d", F3C_MAX_BATCH);
   if (!q_off_host || !k_off_host || !q || !k || !v || !o) return fail(F3C_EINVAL, "NULL argument");
@@ -1005,7 +1007,7 @@ int f3c_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int32_t bat
       return fail(F3C_EINVAL, "sample %d has queries but no keys", b);
   if (workspace && ((uintptr_t)workspace & 15)) return fail(F3C_EINVAL, "workspace must be 16-byte aligned");
   HIP_TRY(launch_attention(SITE_OP, dtype, heads, head_dim, qs, ks, q, ldq, k, ldk, v, ldv, o, ldo, workspace,
-                           workspace ? workspace_bytes : 0, (hipStream_t)stream));
+                           workspace ? workspace_bytes : 0, (hipStream_t)stream, q_prescaled == 1));
   return F3C_OK;
 }
 

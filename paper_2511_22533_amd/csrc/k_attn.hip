@@ -11,6 +11,12 @@
 // B operand without any data movement; the K-slot order of P (keys
 // 8*(e/4) + 4*(l/32) + e%4) is matched when the V^T fragment is read.
 //
+// Scores on the matrix-core path (bf16, 64-wide heads) come out of the MFMAs
+// already shifted: each score tile's accumulation starts from -m (the
+// reference max), so a probability costs one exponential (and, unless the
+// queries were stored multiplied by log2(e)/sqrt(hd), one multiply) plus its
+// bf16 conversion.
+//
 // Pipelining. bf16 with 64-wide heads (the transformer's case): K and V tiles
 // go from global memory straight into four LDS buffers with 16-byte DMA loads
 // issued three tiles ahead, and the score product of tile t+1 is issued before
@@ -86,7 +92,7 @@ struct AttnArgs {
   char* o;
   int ldq, ldk, ldv, ldo;        // elements
   int heads;
-  float scale_log2;              // log2(e) / sqrt(hd)
+  float scale_log2;              // log2(e) / sqrt(hd), or 1 when the queries were stored scaled by it
   int splits;                    // key-range splits (1: normalised output straight to o)
   int rows;                      // query rows qs.off[B] - qs.off[0] (split partials)
   float* part_o;                 // [splits][rows][heads][hd] unnormalised outputs
@@ -99,7 +105,9 @@ struct AttnArgs {
 // groups' (max, sum, output) are merged through LDS at the end. Two groups
 // double the waves per query tile where query tiles are too few to fill the
 // chip.
-template <typename T, int HD, int NW, int SITE, bool SPLIT, int KS = 1>
+// QS: the queries were stored multiplied by log2(e)/sqrt(hd) (scores come out
+// in base-2 units).
+template <typename T, int HD, int NW, int SITE, bool SPLIT, int KS = 1, bool QS = false>
 __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
   constexpr int NT = 64 * NW;
   constexpr int QW = NW / KS;                // query waves
@@ -384,6 +392,9 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
     // peeled. Probabilities use a reference max that moves only in the rare
     // fix-up branch (kTileSumLimit), so no per-tile max is computed.
     const bf16x2 ones = {(bf16)1.0f, (bf16)1.0f};
+    f32x16 minit;                        // -(reference max) * c in every slot
+#pragma unroll
+    for (int e = 0; e < 16; ++e) minit[e] = 0.0f;
     auto qk2 = [&](int buf, f32x16 (&s)[2]) {
       const char* Ks = lds + buf * SB + kgrp * TB;
       u32x4 kf[2][NKS];
@@ -397,7 +408,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
           s[kt] = Mfma<T>::mma(__builtin_bit_cast(bf16x8, kf[kt][q]), __builtin_bit_cast(bf16x8, qf[q]),
-                               q == 0 ? f32x16{} : s[kt]);
+                               q == 0 ? minit : s[kt]);
     };
     // O^T += V^T P^T for the tile in buffer buf; keys kb..kb+3 and kb+8..kb+11
     // at column h*32 + (lane%32) through two transpose reads of the row-major
@@ -429,20 +440,20 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
             if (kv0 + kt * 32 + 8 * (e >> 2) + 4 * g + (e & 3) >= nk) s[kt][e] = -INFINITY;
       }
     };
-    // Probabilities 2^((s - m_run) c) as the bf16 P fragments; returns their
+    // Probabilities 2^((s - m_run) c) as the bf16 P fragments (the shift is
+    // already in the accumulators; c is 1 with pre-scaled queries); returns their
     // sum as rounded for the PV product (v_dot2 with ones).
     auto probs = [&](const f32x16 (&s)[2], bf16x8 (&pf)[2][2]) {
       // with key groups a group's only tile can lie past the end (all keys
       // masked, max -inf): its probabilities are then 0
-      float mc = m_run * c;
-      if constexpr (KS > 1) mc = m_run == -INFINITY ? 0.0f : mc;
       float part[4];                     // four independent accumulation chains
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
 #pragma unroll
-          for (int e = 0; e < 8; ++e) pf[kt][u][e] = (bf16)__builtin_amdgcn_exp2f(fmaf(s[kt][8 * u + e], c, -mc));
+          for (int e = 0; e < 8; ++e)
+            pf[kt][u][e] = (bf16)__builtin_amdgcn_exp2f(QS ? s[kt][8 * u + e] : s[kt][8 * u + e] * c);
           const bf16x8& f = pf[kt][u];
           float a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(f, f, 0, 1), ones, 0.0f, false);
           a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(f, f, 2, 3), ones, a, false);
@@ -460,16 +471,26 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
     // Rare: some lane's probabilities outgrew the reference; move it to the
     // tile's max, rescale what was accumulated (including the PV product of
     // the previous tile, issued before) and redo the tile.
-    auto fixup = [&](const f32x16 (&s)[2], bf16x8 (&pf)[2][2], float& lt) {
+    auto fixup = [&](f32x16 (&s)[2], f32x16* next, bf16x8 (&pf)[2][2], float& lt) {
       if (__builtin_amdgcn_ballot_w64(lt > kTileSumLimit) != 0) {
-        const float m_new = fmaxf(m_run, tile_max(s));
-        const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c);
-        m_run = m_new;
+        const float tm = fmaxf(tile_max(s), 0.0f);   // tile max above the reference
+        const float alpha = __builtin_amdgcn_exp2f(QS ? -tm : -tm * c);
+        m_run += tm;
         l_run *= alpha;
 #pragma unroll
         for (int u = 0; u < HT; ++u)
 #pragma unroll
           for (int e = 0; e < 16; ++e) oacc[u][e] *= alpha;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          minit[e] = -m_run;
+          s[0][e] -= tm;
+          s[1][e] -= tm;
+          if (next) {
+            next[0][e] -= tm;
+            next[1][e] -= tm;
+          }
+        }
         lt = probs(s, pf);
       }
     };
@@ -495,7 +516,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
       qk2(bnext(buf, 1), next);
       if constexpr (!decltype(first)::value) pv2(bnext(buf, NBUF - 1), pprev);
       float lt = probs(cur, pcur);
-      fixup(cur, pcur, lt);
+      fixup(cur, next, pcur, lt);
       l_run += lt;
     };
     // Last step i (its tiles maybe ragged or past the end): PV(i-1), P(i), then PV(i).
@@ -504,7 +525,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
       if constexpr (!decltype(first)::value) pv2(bnext(buf, NBUF - 1), pprev);
       mask2(tile_of(i), cur);
       float lt = probs(cur, pcur);
-      fixup(cur, pcur, lt);
+      fixup(cur, nullptr, pcur, lt);
       l_run += lt;
       pv2(buf, pcur);
     };
@@ -522,6 +543,15 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
       qk2(0, sa);
       if (n_steps == 1) mask2(tile_of(0), sa);
       m_run = tile_max(sa);              // reference max: the first tile's
+      {
+        const float sub = m_run == -INFINITY ? 0.0f : m_run;   // a key group's tile may lie past the end
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          minit[e] = -sub;
+          sa[0][e] -= sub;
+          sa[1][e] -= sub;
+        }
+      }
       const std::true_type yes{};
       const std::false_type no{};
       if (n_steps == 1) {
@@ -667,19 +697,19 @@ __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs p) {
   }
 }
 
-template <typename T, int HD, int NW, int SITE, int KS = 1>
+template <typename T, int HD, int NW, int SITE, int KS = 1, bool QS = false>
 hipError_t launch_k(const AttnArgs& a, int tiles, hipStream_t s) {
   const dim3 block(64 * NW);
   if constexpr (KS > 1) {
     if (a.splits != 1) return hipErrorInvalidValue;
-    launch((k_attn<T, HD, NW, SITE, false, KS>), dim3(tiles * a.heads), block, 0, s, a);
+    launch((k_attn<T, HD, NW, SITE, false, KS, QS>), dim3(tiles * a.heads), block, 0, s, a);
     return hipGetLastError();
   }
   if (a.splits == 1) {
-    launch((k_attn<T, HD, NW, SITE, false>), dim3(tiles * a.heads), block, 0, s, a);
+    launch((k_attn<T, HD, NW, SITE, false, 1, QS>), dim3(tiles * a.heads), block, 0, s, a);
     return hipGetLastError();
   }
-  launch((k_attn<T, HD, NW, SITE, true>), dim3(tiles * a.heads * a.splits), block, 0, s, a);
+  launch((k_attn<T, HD, NW, SITE, true, 1, QS>), dim3(tiles * a.heads * a.splits), block, 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int64_t n = (int64_t)a.rows * a.heads * (HD / 4);
@@ -689,7 +719,7 @@ hipError_t launch_k(const AttnArgs& a, int tiles, hipStream_t s) {
 
 // splits > 1 requires a.part_o / a.part_ml sized for them.
 template <int NW, int SITE, int KS = 1>
-hipError_t launch_a(int dt, int hd, const AttnArgs& a0, int heads, int splits, hipStream_t s) {
+hipError_t launch_a(int dt, int hd, const AttnArgs& a0, int heads, int splits, hipStream_t s, bool qs) {
   AttnArgs a = a0;
   constexpr int BQ = 32 * NW / KS;
   a.tile_off[0] = 0;
@@ -700,10 +730,12 @@ hipError_t launch_a(int dt, int hd, const AttnArgs& a0, int heads, int splits, h
   a.splits = splits;
   a.rows = a.qs.off[a.qs.B] - a.qs.off[0];
   if constexpr (KS > 1) {
-    if (dt == DT_BF16 && hd == 64) return launch_k<bf16, 64, NW, SITE, KS>(a, tiles, s);
+    if (dt == DT_BF16 && hd == 64)
+      return qs ? launch_k<bf16, 64, NW, SITE, KS, true>(a, tiles, s) : launch_k<bf16, 64, NW, SITE, KS>(a, tiles, s);
     return hipErrorInvalidValue;
   } else {
-    if (dt == DT_BF16 && hd == 64) return launch_k<bf16, 64, NW, SITE>(a, tiles, s);
+    if (dt == DT_BF16 && hd == 64)
+      return qs ? launch_k<bf16, 64, NW, SITE, 1, true>(a, tiles, s) : launch_k<bf16, 64, NW, SITE>(a, tiles, s);
     if (dt == DT_BF16 && hd == 32) return launch_k<bf16, 32, NW, SITE>(a, tiles, s);
     if (dt == DT_F32 && hd == 64) return launch_k<float, 64, NW, SITE>(a, tiles, s);
     if (dt == DT_F32 && hd == 32) return launch_k<float, 32, NW, SITE>(a, tiles, s);
@@ -737,7 +769,8 @@ inline size_t split_bytes(int splits, int rows, int heads, int hd) {
 constexpr long kSplitGainTiles = 5;
 
 template <int SITE>
-hipError_t launch_site(int dt, int hd, const AttnArgs& a, int heads, float* ws, size_t ws_bytes, hipStream_t s) {
+hipError_t launch_site(int dt, int hd, const AttnArgs& a, int heads, float* ws, size_t ws_bytes, hipStream_t s,
+                       bool qs) {
   long t64 = 0, t128 = 0, t256 = 0, kt_min = 1L << 30, kt_max = 0;
   for (int b = 0; b < a.qs.B; ++b) {
     const int nq = a.qs.off[b + 1] - a.qs.off[b];
@@ -749,28 +782,28 @@ hipError_t launch_site(int dt, int hd, const AttnArgs& a, int heads, float* ws, 
     kt_min = std::min(kt_min, kt);
     kt_max = std::max(kt_max, kt);
   }
-  if (t256 * heads >= 160) return launch_a<8, SITE>(dt, hd, a, heads, 1, s);
+  if (t256 * heads >= 160) return launch_a<8, SITE>(dt, hd, a, heads, 1, s, qs);
   int splits = 1;
   while (splits < 8 && t128 * heads * splits * 2 <= 256 && kt_min >= 16 * splits) splits *= 2;
   const int rows = a.qs.off[a.qs.B] - a.qs.off[0];
   while (splits > 1 && (!ws || split_bytes(splits, rows, heads, hd) > ws_bytes)) splits /= 2;
   if (dt == DT_BF16 && hd == 64 && (kt_max + 1) / 2 - (kt_max + splits - 1) / splits <= kSplitGainTiles) {
-    if (t64 * heads <= 256) return launch_a<4, SITE, 2>(dt, hd, a, heads, 1, s);
-    return launch_a<8, SITE, 2>(dt, hd, a, heads, 1, s);
+    if (t64 * heads <= 256) return launch_a<4, SITE, 2>(dt, hd, a, heads, 1, s, qs);
+    return launch_a<8, SITE, 2>(dt, hd, a, heads, 1, s, qs);
   }
   AttnArgs b = a;
   if (splits > 1) {
     b.part_o = ws;
     b.part_ml = ws + (size_t)splits * rows * heads * hd;
   }
-  return launch_a<4, SITE>(dt, hd, b, heads, splits, s);
+  return launch_a<4, SITE>(dt, hd, b, heads, splits, s, qs);
 }
 
 }  // namespace
 
 hipError_t launch_attention(int site, int dt, int heads, int hd, const Segs& qs, const Segs& ks, const void* q,
                             int ldq, const void* k, int ldk, const void* v, int ldv, void* o, int ldo, float* ws,
-                            size_t ws_bytes, hipStream_t s) {
+                            size_t ws_bytes, hipStream_t s, bool q_scaled) {
   AttnArgs a;
   a.qs = qs;
   a.ks = ks;
@@ -782,12 +815,12 @@ hipError_t launch_attention(int site, int dt, int heads, int hd, const Segs& qs,
   a.ldk = ldk;
   a.ldv = ldv;
   a.ldo = ldo;
-  a.scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
+  a.scale_log2 = q_scaled ? 1.0f : attention_q_scale(hd);
   a.splits = 1;
   a.part_o = a.part_ml = nullptr;
-  if (site == SITE_SELF) return launch_site<SITE_SELF>(dt, hd, a, heads, ws, ws_bytes, s);
-  if (site == SITE_CROSS) return launch_site<SITE_CROSS>(dt, hd, a, heads, ws, ws_bytes, s);
-  return launch_site<SITE_OP>(dt, hd, a, heads, ws, ws_bytes, s);
+  if (site == SITE_SELF) return launch_site<SITE_SELF>(dt, hd, a, heads, ws, ws_bytes, s, q_scaled);
+  if (site == SITE_CROSS) return launch_site<SITE_CROSS>(dt, hd, a, heads, ws, ws_bytes, s, q_scaled);
+  return launch_site<SITE_OP>(dt, hd, a, heads, ws, ws_bytes, s, q_scaled);
 }
 
 }  // namespace f3c

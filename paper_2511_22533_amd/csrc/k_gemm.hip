@@ -44,6 +44,8 @@ struct GemmArgs {
   float* resid;
   int ldr;
   int xq;                             // column groups of the XCD tile partition (divides N / BN)
+  float oscale;                       // stored outputs of columns < oscale_cols are multiplied by oscale
+  int oscale_cols;
 };
 
 template <typename T>
@@ -258,6 +260,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(GemmArgs p) {
 #pragma unroll
             for (int e = 0; e < 4; ++e) v[e] = gelu_tanh(v[e]);
           }
+          if (col < p.oscale_cols) {        // four columns: all in or all out (oscale_cols % 4 == 0)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] *= p.oscale;
+          }
           store4<T>(reinterpret_cast<T*>(p.out) + (size_t)row * p.ldo + col, v);
         }
       }
@@ -450,6 +456,10 @@ __global__ __launch_bounds__(64 * NW) void k_gemm2(GemmArgs p) {
 #pragma unroll
           for (int e = 0; e < 4; ++e) v[e] = gelu_tanh(v[e]);
         }
+        if (col < p.oscale_cols) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] *= p.oscale;
+        }
         store4<bf16>(reinterpret_cast<bf16*>(p.out) + (size_t)row * p.ldo + col, v);
       }
     }
@@ -576,9 +586,11 @@ hipError_t launch_site(int site, int epi, const GemmArgs& a, hipStream_t s) {
 
 hipError_t launch_gemm(int site, int dt, int epi, int M, int N, int K, const void* A, int lda, const void* W,
                        int ldw, const float* bias, const float* gate, void* out, int ldo, float* resid, int ldr,
-                       hipStream_t s) {
+                       hipStream_t s, float oscale, int oscale_cols) {
   if (M == 0) return hipSuccess;
-  GemmArgs a{M, N, K, (const char*)A, lda, (const char*)W, ldw, bias, gate, out, ldo, resid, ldr, 1};
+  if (oscale_cols % 4) return hipErrorInvalidValue;
+  GemmArgs a{M, N, K, (const char*)A, lda, (const char*)W, ldw, bias, gate, out, ldo, resid, ldr, 1, oscale,
+             oscale_cols};
   return dt == DT_BF16 ? launch_site<bf16>(site, epi, a, s) : launch_site<float>(site, epi, a, s);
 }
 

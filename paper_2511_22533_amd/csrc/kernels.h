@@ -3,6 +3,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <math.h>
 #include <stdint.h>
 
 namespace f3c {
@@ -90,18 +91,26 @@ hipError_t launch_convert(int dt, const float* src, void* dst, int64_t n, hipStr
 // EPI_RESID does resid[m][n] += (gate ? gate[n] : 1) * value in f32.
 // Requires N % 128 == 0 and K % (128 / sizeof(element)) == 0. Each output is
 // one workgroup's sum in a fixed order.
+// EPI_STORE / EPI_GELU with oscale_cols > 0: output columns below oscale_cols
+// are multiplied by oscale after the bias, before the store (the attention's
+// pre-scaled queries).
 hipError_t launch_gemm(int site, int dt, int epi, int M, int N, int K, const void* A, int lda, const void* W,
                        int ldw, const float* bias, const float* gate, void* out, int ldo, float* resid, int ldr,
-                       hipStream_t s);
+                       hipStream_t s, float oscale = 1.0f, int oscale_cols = 0);
 
 // Varlen multi-head softmax attention. Queries of sample b are rows
 // [qs.off[b], qs.off[b+1]) of q; its keys/values are rows [ks.off[b], ks.off[b+1])
 // of k and v. Head h uses columns [h*hd, (h+1)*hd). Output rows match queries.
 // ws (f32, ws_bytes, 16-byte aligned) may be null; when present, launches
 // with few query tiles split the key range and merge the splits through it.
+// q_scaled: the queries were stored multiplied by attention_q_scale(hd)
+// (the step's Q projections do so in their epilogue).
 hipError_t launch_attention(int site, int dt, int heads, int hd, const Segs& qs, const Segs& ks, const void* q,
                             int ldq, const void* k, int ldk, const void* v, int ldv, void* o, int ldo, float* ws,
-                            size_t ws_bytes, hipStream_t s);
+                            size_t ws_bytes, hipStream_t s, bool q_scaled = false);
+
+// log2(e) / sqrt(hd): the softmax scale in base-2 units.
+inline float attention_q_scale(int hd) { return 1.4426950408889634f / sqrtf((float)hd); }
 
 // Occupancy bits from decoder logits (occupied when > 0) for B grids of
 // n_voxels: bits [B][ceil(n_voxels / 32)] u32, voxel n in bit n % 32 of word n / 32.

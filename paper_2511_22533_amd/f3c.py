@@ -85,7 +85,7 @@ _SIGS = {
     "f3c_op_gemm": (c_int, [c_int, c_int, c_int, c_int, c_int, c_p, c_int, c_p, c_int, c_p, c_p, c_p, c_int, c_p,
                             c_int, c_p]),
     "f3c_op_attention": (c_int, [c_int, c_int, c_int, c_int, P_i32, P_i32, c_p, c_int, c_p, c_int, c_p, c_int, c_p,
-                                 c_int, c_p, c_sz, c_p]),
+                                 c_int, c_p, c_sz, c_int, c_p]),
     "f3c_op_ln_mod": (c_int, [c_int, c_int, c_int, c_p, c_p, c_p, c_p, c_p]),
     "f3c_op_modulation": (c_int, [c_p, c_d, c_p, c_p, c_p]),
     "f3c_op_embed": (c_int, [c_p, c_int, c_p, c_p, P_i32, c_p, c_p]),
@@ -458,12 +458,19 @@ def op_gemm(dtype: int, epilogue: int, A, W, bias, out=None, resid=None, gate=No
                             _ptr(resid), resid.stride(0) if resid is not None else 0, _stream(stream)))
 
 
-def op_attention(dtype: int, heads: int, head_dim: int, q_off, k_off, q, k, v, o, workspace=None, stream=None):
+def attention_q_scale(head_dim: int) -> float:
+    """log2(e) / sqrt(head_dim): the factor of pre-scaled queries (q_prescaled)."""
+    import math
+    return float(np.float32(1.4426950408889634) / np.float32(math.sqrt(head_dim)))
+
+
+def op_attention(dtype: int, heads: int, head_dim: int, q_off, k_off, q, k, v, o, workspace=None, stream=None,
+                 q_prescaled: bool = False):
     B = len(q_off) - 1
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     check(lib().f3c_op_attention(dtype, heads, head_dim, B, _i32(q_off), _i32(k_off), q.data_ptr(), q.stride(0),
                                  k.data_ptr(), k.stride(0), v.data_ptr(), v.stride(0), o.data_ptr(), o.stride(0),
-                                 _ptr(workspace), ws_bytes, _stream(stream)))
+                                 _ptr(workspace), ws_bytes, int(q_prescaled), _stream(stream)))
 
 
 def op_embed(model: "Model", x, act_off, h, idx_active=None, stream=None):

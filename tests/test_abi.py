@@ -141,11 +141,12 @@ def test_op_entry_validation_is_host_side(L):
     assert L.f3c_op_gemm(1, 0, 16, 100, 64, 1, 64, 1, 64, 1, None, 1, 100, None, 0, None) == f3c.F3C_EINVAL
     assert L.f3c_op_gemm(1, 0, 16, 128, 40, 1, 40, 1, 40, 1, None, 1, 128, None, 0, None) == f3c.F3C_EINVAL
     assert L.f3c_op_gemm(1, 0, 16, 128, 64, 1, 64, 1, 64, 1, None, 1, 130, None, 0, None) == f3c.F3C_EINVAL
-    assert L.f3c_op_attention(1, 4, 48, 1, q, q, 1, 192, 1, 192, 1, 192, 1, 192, None, 0, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_attention(1, 4, 48, 1, q, q, 1, 192, 1, 192, 1, 192, 1, 192, None, 0, 0, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_attention(1, 4, 64, 1, q, q, 16, 256, 16, 256, 16, 256, 16, 256, None, 0, 2, None) == f3c.F3C_EINVAL
     assert L.f3c_op_attention(1, 4, 64, 1, f3c._i32([0, 3]), f3c._i32([0, 0]), 1, 256, 1, 256, 1, 256, 1, 256,
-                              None, 0, None) == f3c.F3C_EINVAL
+                              None, 0, 0, None) == f3c.F3C_EINVAL
     assert L.f3c_op_attention(1, 4, 64, 1, f3c._i32([0, 3]), f3c._i32([0, 3]), 16, 256, 16, 256, 16, 256, 16, 256,
-                              4, 1024, None) == f3c.F3C_EINVAL
+                              4, 1024, 0, None) == f3c.F3C_EINVAL
     assert b"16-byte aligned" in L.f3c_last_error()
     assert L.f3c_op_ln_mod(1, 4, 96, 1, None, None, 1, None) == f3c.F3C_EINVAL
     assert b"unsupported d" in L.f3c_last_error()

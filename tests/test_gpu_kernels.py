@@ -164,9 +164,12 @@ def test_gemm_f32(torch, M, N, K, epi):
 
 
 def _attn_case(torch, dt, heads, hd, q_lens, k_lens, seed, sample_queries=None, workspace=False, outputs=None,
-               key_ramp=0.0):
+               key_ramp=0.0, prescaled=False):
     """key_ramp > 0 scales key j of each sample by 1 + key_ramp * (j // 64): every
-    64-key tile then has larger scores than the ones before it."""
+    64-key tile then has larger scores than the ones before it. prescaled: the
+    queries go in multiplied by log2(e)/sqrt(hd) (rounded once, as the step's
+    projections store them) and the reference takes the stored values divided
+    by that factor."""
     from paper_2511_22533_amd import f3c
     rng = np.random.default_rng(seed)
     d = heads * hd
@@ -179,13 +182,16 @@ def _attn_case(torch, dt, heads, hd, q_lens, k_lens, seed, sample_queries=None, 
         j = np.concatenate([np.arange(n) for n in k_lens]) if k_off[-1] else np.zeros(0, int)
         k *= (1.0 + key_ramp * (j // 64)).astype(np.float32)[:, None]
     tdt = torch.bfloat16 if dt == f3c.F3C_BF16 else torch.float32
+    cq = f3c.attention_q_scale(hd) if prescaled else 1.0
+    q_in = (q * np.float32(cq)).astype(np.float32)
     if dt == f3c.F3C_BF16:
-        q, k, v = bf16_round(q), bf16_round(k), bf16_round(v)
+        q_in, k, v = bf16_round(q_in), bf16_round(k), bf16_round(v)
+    q = (q_in.astype(np.float64) / cq) if prescaled else q_in     # what the kernel's input means
     o = torch.zeros((max(q_off[-1], 1), d), dtype=tdt, device="cuda")
     ws = torch.empty(8 << 20, dtype=torch.float32, device="cuda") if workspace else None
     say("attention", dt, heads, hd, list(q_lens), list(k_lens), "workspace" if workspace else "")
-    f3c.op_attention(dt, heads, hd, q_off.tolist(), k_off.tolist(), to_dev(q, tdt), to_dev(k, tdt),
-                     to_dev(v, tdt), o, workspace=ws)
+    f3c.op_attention(dt, heads, hd, q_off.tolist(), k_off.tolist(), to_dev(q_in, tdt), to_dev(k, tdt),
+                     to_dev(v, tdt), o, workspace=ws, q_prescaled=prescaled)
     torch.cuda.synchronize()
     got = o.float().cpu().numpy()
     if outputs is not None:
@@ -210,21 +216,27 @@ def _attn_case(torch, dt, heads, hd, q_lens, k_lens, seed, sample_queries=None, 
 @pytest.mark.parametrize("q_lens,k_lens", [([64], [64]), ([1], [1]), ([200], [200]), ([0, 37, 300], [0, 37, 300]),
                                            ([820], [820]), ([615, 1536, 2458, 1003], [615, 1536, 2458, 1003]),
                                            ([1024], [1024]), ([1025], [1025])])
-def test_self_attention_bf16(torch, q_lens, k_lens):
+@pytest.mark.parametrize("prescaled", [False, True])
+def test_self_attention_bf16(torch, q_lens, k_lens, prescaled):
     from paper_2511_22533_amd import f3c
-    assert _attn_case(torch, f3c.F3C_BF16, 16, 64, q_lens, k_lens, seed=sum(q_lens)) < 2e-2
+    assert _attn_case(torch, f3c.F3C_BF16, 16, 64, q_lens, k_lens, seed=sum(q_lens), prescaled=prescaled) < 2e-2
 
 
-def test_self_attention_bf16_full_size_sampled(torch):
+@pytest.mark.parametrize("prescaled", [False, True])
+def test_self_attention_bf16_full_size_sampled(torch, prescaled):
     from paper_2511_22533_amd import f3c
-    assert _attn_case(torch, f3c.F3C_BF16, 16, 64, [4096], [4096], seed=5, sample_queries=96) < 2e-2
-    assert _attn_case(torch, f3c.F3C_BF16, 16, 64, [9831], [9831], seed=6, sample_queries=64) < 2e-2
+    assert _attn_case(torch, f3c.F3C_BF16, 16, 64, [4096], [4096], seed=5, sample_queries=96,
+                      prescaled=prescaled) < 2e-2
+    assert _attn_case(torch, f3c.F3C_BF16, 16, 64, [9831], [9831], seed=6, sample_queries=64,
+                      prescaled=prescaled) < 2e-2
 
 
 @pytest.mark.parametrize("q_lens", [[820], [5, 1000, 0, 77]])
-def test_cross_attention_bf16(torch, q_lens):
+@pytest.mark.parametrize("prescaled", [False, True])
+def test_cross_attention_bf16(torch, q_lens, prescaled):
     from paper_2511_22533_amd import f3c
-    assert _attn_case(torch, f3c.F3C_BF16, 16, 64, q_lens, [1374] * len(q_lens), seed=len(q_lens)) < 2e-2
+    assert _attn_case(torch, f3c.F3C_BF16, 16, 64, q_lens, [1374] * len(q_lens), seed=len(q_lens),
+                      prescaled=prescaled) < 2e-2
 
 
 # With a workspace, launches with few query tiles may split the key range
@@ -236,12 +248,13 @@ def test_cross_attention_bf16(torch, q_lens):
 @pytest.mark.parametrize("q_lens,k_lens", [([1000], [1000]), ([820], [1374]), ([5, 300, 0, 77], [1374] * 4),
                                            ([300], [1374]), ([1, 40], [4096, 2000]), ([64], [8192]),
                                            ([1310], [1310]), ([820], [820])])
-def test_attention_bf16_split_keys(torch, q_lens, k_lens):
+@pytest.mark.parametrize("prescaled", [False, True])
+def test_attention_bf16_split_keys(torch, q_lens, k_lens, prescaled):
     from paper_2511_22533_amd import f3c
     outs = []
     for rep in range(2):
         assert _attn_case(torch, f3c.F3C_BF16, 16, 64, q_lens, k_lens, seed=sum(k_lens), workspace=True,
-                          outputs=outs) < 2e-2
+                          outputs=outs, prescaled=prescaled) < 2e-2
     assert np.array_equal(outs[0], outs[1])
 
 
@@ -253,10 +266,11 @@ def test_attention_bf16_split_keys(torch, q_lens, k_lens):
 @pytest.mark.parametrize("q_lens,k_lens,ramp,ws", [([300], [300], 2.0, False), ([1000], [1000], 0.5, False),
                                                    ([820], [1374], 1.0, False), ([300], [4096], 0.5, True),
                                                    ([37, 3000], [37, 3000], 0.3, False), ([640], [640], 0.12, False)])
-def test_attention_bf16_growing_scores(torch, q_lens, k_lens, ramp, ws):
+@pytest.mark.parametrize("prescaled", [False, True])
+def test_attention_bf16_growing_scores(torch, q_lens, k_lens, ramp, ws, prescaled):
     from paper_2511_22533_amd import f3c
     assert _attn_case(torch, f3c.F3C_BF16, 16, 64, q_lens, k_lens, seed=int(10 * ramp) + len(q_lens),
-                      workspace=ws, key_ramp=ramp, sample_queries=128) < 2e-2
+                      workspace=ws, key_ramp=ramp, sample_queries=128, prescaled=prescaled) < 2e-2
 
 
 # Two key groups with one or two key tiles: the second group's only tile lies
@@ -264,9 +278,10 @@ def test_attention_bf16_growing_scores(torch, q_lens, k_lens, ramp, ws):
 # workgroups up to 1024 queries, eight-wave ones at 1100.
 @pytest.mark.parametrize("q_lens,k_lens", [([600], [50]), ([600], [64]), ([700], [100]), ([5, 600], [1, 65]),
                                            ([1100], [50]), ([1100], [100])])
-def test_attention_bf16_key_groups_short_keys(torch, q_lens, k_lens):
+@pytest.mark.parametrize("prescaled", [False, True])
+def test_attention_bf16_key_groups_short_keys(torch, q_lens, k_lens, prescaled):
     from paper_2511_22533_amd import f3c
-    assert _attn_case(torch, f3c.F3C_BF16, 16, 64, q_lens, k_lens, seed=sum(k_lens)) < 2e-2
+    assert _attn_case(torch, f3c.F3C_BF16, 16, 64, q_lens, k_lens, seed=sum(k_lens), prescaled=prescaled) < 2e-2
 
 
 @pytest.mark.parametrize("hd,heads", [(32, 4), (64, 2)])
@@ -278,9 +293,11 @@ def test_attention_f32_split_keys(torch, hd, heads):
 
 @pytest.mark.parametrize("hd,heads", [(32, 4), (64, 2)])
 @pytest.mark.parametrize("q_lens,k_lens", [([512], [512]), ([3, 256, 130], [64, 64, 64]), ([100], [1])])
-def test_attention_f32(torch, hd, heads, q_lens, k_lens):
+@pytest.mark.parametrize("prescaled", [False, True])
+def test_attention_f32(torch, hd, heads, q_lens, k_lens, prescaled):
     from paper_2511_22533_amd import f3c
-    assert _attn_case(torch, f3c.F3C_F32, heads, hd, q_lens, k_lens, seed=hd + len(q_lens)) < 1e-4
+    assert _attn_case(torch, f3c.F3C_F32, heads, hd, q_lens, k_lens, seed=hd + len(q_lens),
+                      prescaled=prescaled) < 1e-4
 
 
 def test_attention_f32_eight_waves_sampled(torch):
