@@ -466,6 +466,199 @@ __global__ __launch_bounds__(64 * NW) void k_gemm2(GemmArgs p) {
   }
 }
 
+// Large projections (tens of thousands of rows): 256 x 256 tiles of 8 waves,
+// each owning a 128 x 64 block (4 x 2 accumulators of 32 x 32), two waves per
+// SIMD. K tiles of 64 elements go HBM -> LDS by DMA into two stages (XOR
+// swizzled 128-byte rows as in k_gemm2). Each 16-element K-step is one
+// inline-assembly block: it waits for its own fragments, then interleaves the
+// six fragment reads of the next K-step with its eight MFMAs, so LDS latency
+// stays behind matrix work without depending on the compiler's schedule.
+// Before the last K-step of a tile every wave holds that step's fragments, so
+// one barrier (after the DMA of the next tile landed) retires the tile's
+// stage, which then receives the tile after next, and makes the next tile
+// readable: the last K-step already reads the next tile's first fragments.
+// Same K order and instruction as k_gemm, so its results are bit-identical.
+// Requires N % 256 == 0 and K % 128 == 0 (an even number of K tiles).
+// K-step with prefetch: acc[i][j] += W[j] A[i] (i < 4, j < 2), and the six
+// fragments of the next K-step read into the other register set.
+#define G3_STEP_PF(C, FA, FW, NA, NW, AAD, WAD)                                                                \
+  asm volatile("s_waitcnt lgkmcnt(0)\n\t"                                                                      \
+               "ds_read_b128 %[na0], %[aad]\n\t"                                                               \
+               "v_mfma_f32_32x32x16_bf16 %[c00], %[w0], %[a0], %[c00]\n\t"                                     \
+               "ds_read_b128 %[na1], %[aad] offset:4096\n\t"                                                   \
+               "v_mfma_f32_32x32x16_bf16 %[c01], %[w1], %[a0], %[c01]\n\t"                                     \
+               "ds_read_b128 %[na2], %[aad] offset:8192\n\t"                                                   \
+               "v_mfma_f32_32x32x16_bf16 %[c10], %[w0], %[a1], %[c10]\n\t"                                     \
+               "ds_read_b128 %[na3], %[aad] offset:12288\n\t"                                                  \
+               "v_mfma_f32_32x32x16_bf16 %[c11], %[w1], %[a1], %[c11]\n\t"                                     \
+               "ds_read_b128 %[nw0], %[wad]\n\t"                                                               \
+               "v_mfma_f32_32x32x16_bf16 %[c20], %[w0], %[a2], %[c20]\n\t"                                     \
+               "ds_read_b128 %[nw1], %[wad] offset:4096\n\t"                                                   \
+               "v_mfma_f32_32x32x16_bf16 %[c21], %[w1], %[a2], %[c21]\n\t"                                     \
+               "v_mfma_f32_32x32x16_bf16 %[c30], %[w0], %[a3], %[c30]\n\t"                                     \
+               "v_mfma_f32_32x32x16_bf16 %[c31], %[w1], %[a3], %[c31]"                                         \
+               : [c00] "+v"(C[0][0]), [c01] "+v"(C[0][1]), [c10] "+v"(C[1][0]), [c11] "+v"(C[1][1]),            \
+                 [c20] "+v"(C[2][0]), [c21] "+v"(C[2][1]), [c30] "+v"(C[3][0]), [c31] "+v"(C[3][1]),            \
+                 [na0] "=&v"(NA[0]), [na1] "=&v"(NA[1]), [na2] "=&v"(NA[2]), [na3] "=&v"(NA[3]),               \
+                 [nw0] "=&v"(NW[0]), [nw1] "=&v"(NW[1])                                                        \
+               : [a0] "v"(FA[0]), [a1] "v"(FA[1]), [a2] "v"(FA[2]), [a3] "v"(FA[3]), [w0] "v"(FW[0]),          \
+                 [w1] "v"(FW[1]), [aad] "v"(AAD), [wad] "v"(WAD))
+
+#define G3_STEP(C, FA, FW)                                                                                     \
+  asm volatile("s_waitcnt lgkmcnt(0)\n\t"                                                                      \
+               "v_mfma_f32_32x32x16_bf16 %[c00], %[w0], %[a0], %[c00]\n\t"                                     \
+               "v_mfma_f32_32x32x16_bf16 %[c01], %[w1], %[a0], %[c01]\n\t"                                     \
+               "v_mfma_f32_32x32x16_bf16 %[c10], %[w0], %[a1], %[c10]\n\t"                                     \
+               "v_mfma_f32_32x32x16_bf16 %[c11], %[w1], %[a1], %[c11]\n\t"                                     \
+               "v_mfma_f32_32x32x16_bf16 %[c20], %[w0], %[a2], %[c20]\n\t"                                     \
+               "v_mfma_f32_32x32x16_bf16 %[c21], %[w1], %[a2], %[c21]\n\t"                                     \
+               "v_mfma_f32_32x32x16_bf16 %[c30], %[w0], %[a3], %[c30]\n\t"                                     \
+               "v_mfma_f32_32x32x16_bf16 %[c31], %[w1], %[a3], %[c31]"                                         \
+               : [c00] "+v"(C[0][0]), [c01] "+v"(C[0][1]), [c10] "+v"(C[1][0]), [c11] "+v"(C[1][1]),            \
+                 [c20] "+v"(C[2][0]), [c21] "+v"(C[2][1]), [c30] "+v"(C[3][0]), [c31] "+v"(C[3][1])             \
+               : [a0] "v"(FA[0]), [a1] "v"(FA[1]), [a2] "v"(FA[2]), [a3] "v"(FA[3]), [w0] "v"(FW[0]),          \
+                 [w1] "v"(FW[1]))
+
+template <int EPI, int SITE>
+__global__ __launch_bounds__(512) void k_gemm_big(GemmArgs p) {
+  constexpr int BM = 256, BN = 256, KTB = 128, SBUF = (BM + BN) * KTB, ABUF = BM * KTB;
+  __shared__ __attribute__((aligned(16))) char lds[2 * SBUF];   // 128 KiB
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 2, wn = wave & 3;                      // 128-row half, 64-column quarter
+  const int g = lane >> 5, r32 = lane & 31;
+  int n0, m0;
+  {
+    const int gx = p.N / BN, gy = (p.M + BM - 1) / BM;
+    const int l = xcd_logical_id(blockIdx.x, gx * gy);
+    const int gq = gx / p.xq, per_group = gy * gq;
+    const int grp = l / per_group, r = l - grp * per_group;
+    const int y = r / gq;
+    n0 = (grp * gq + (r - y * gq)) * BN;
+    m0 = y * BM;
+  }
+  const size_t lda_b = (size_t)p.lda * 2, ldw_b = (size_t)p.ldw * 2;
+  const int KT = (p.K * 2) / KTB;
+  // DMA: 64 blocks of 1 KiB (8 rows of 128 bytes) per tile: A rows 8b.. for
+  // b < 32, W rows 8(b-32).. for b >= 32; wave w takes blocks w, w+8, ...
+  // Lane l fills row 8b + l/8 at physical chunk l%8 with the logical chunk the
+  // row's swizzle ((row >> 1) & 7) maps there.
+  const char* dsrc[8];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    const int blk = wave + 8 * q;
+    const int phys = lane & 7, rr = lane >> 3;
+    if (blk < 32) {
+      const int row = 8 * blk + rr;
+      dsrc[q] = p.A + (size_t)min(m0 + row, p.M - 1) * lda_b + ((phys ^ ((row >> 1) & 7)) << 4);
+    } else {
+      const int row = 8 * (blk - 32) + rr;
+      dsrc[q] = p.W + (size_t)(n0 + row) * ldw_b + ((phys ^ ((row >> 1) & 7)) << 4);
+    }
+  }
+  auto fetch = [&](int kt, int stage) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) dma16(dsrc[q] + (size_t)kt * KTB, lds + stage * SBUF + (wave + 8 * q) * 1024);
+  };
+  // Fragment read bases (bytes): A row wm*128 + r32, W row wn*64 + r32, logical
+  // chunk 2ks + g -> physical (2ks + g) ^ ((r32 >> 1) & 7).
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds;
+  const int swz = (r32 >> 1) & 7;
+  uint32_t aad[2][4], wad[2][4];
+#pragma unroll
+  for (int s = 0; s < 2; ++s)
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const uint32_t ch = (uint32_t)(((2 * ks + g) ^ swz) << 4);
+      aad[s][ks] = lds0 + s * SBUF + (wm * 128 + r32) * KTB + ch;
+      wad[s][ks] = lds0 + s * SBUF + ABUF + (wn * 64 + r32) * KTB + ch;
+    }
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+
+  u32x4 fa[2][4], fw[2][2];
+  auto read_frags = [&](int s) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(fa[0][i]) : "v"(aad[s][0]), "i"(i * 4096));
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+      asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(fw[0][j]) : "v"(wad[s][0]), "i"(j * 4096));
+  };
+  // Tile kt in stage s: K-step ks uses register set ks & 1 and reads the next
+  // step's fragments into the other set. Before the last K-step every wave
+  // holds that step's fragments, so one barrier (after the DMA of tile kt + 1
+  // landed) both retires stage s, which then receives tile kt + 2, and makes
+  // stage s ^ 1 readable: the last K-step reads the first fragments of tile
+  // kt + 1 while its MFMAs run.
+  auto tile = [&](int kt, int s) {
+    G3_STEP_PF(acc, fa[0], fw[0], fa[1], fw[1], aad[s][1], wad[s][1]);
+    G3_STEP_PF(acc, fa[1], fw[1], fa[0], fw[0], aad[s][2], wad[s][2]);
+    G3_STEP_PF(acc, fa[0], fw[0], fa[1], fw[1], aad[s][3], wad[s][3]);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    wait_vm<0>();
+    __syncthreads();
+    fetch(min(kt + 2, KT - 1), s);
+    G3_STEP_PF(acc, fa[1], fw[1], fa[0], fw[0], aad[s ^ 1][0], wad[s ^ 1][0]);
+  };
+  // KT is even (K a multiple of 128).
+  fetch(0, 0);
+  wait_vm<0>();
+  __syncthreads();
+  read_frags(0);
+  fetch(min(1, KT - 1), 1);
+  for (int kt = 0; kt < KT; kt += 2) {
+    tile(kt, 0);
+    tile(kt + 1, 1);
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  wait_vm<0>();
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");   // MFMA results before the reads below
+
+  // Epilogue: block (i, j) of this wave, group q: activation row
+  // m0 + 128 wm + 32 i + r32, output columns n0 + 64 wn + 32 j + 8 q + 4 g + (0..3).
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = m0 + wm * 128 + i * 32 + r32;
+    if (row >= p.M) continue;
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int col = n0 + wn * 64 + j * 32 + 8 * q + 4 * g;
+        const f32x16& c = acc[i][j];
+        const float4 bv = *reinterpret_cast<const float4*>(p.bias + col);
+        float v[4] = {c[4 * q] + bv.x, c[4 * q + 1] + bv.y, c[4 * q + 2] + bv.z, c[4 * q + 3] + bv.w};
+        if constexpr (EPI == EPI_RESID) {
+          float4 gv = make_float4(1.0f, 1.0f, 1.0f, 1.0f);
+          if (p.gate) gv = *reinterpret_cast<const float4*>(p.gate + col);
+          float4* r = reinterpret_cast<float4*>(p.resid + (size_t)row * p.ldr + col);
+          float4 h = *r;
+          h.x += gv.x * v[0];
+          h.y += gv.y * v[1];
+          h.z += gv.z * v[2];
+          h.w += gv.w * v[3];
+          *r = h;
+        } else {
+          if constexpr (EPI == EPI_GELU) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = gelu_tanh(v[e]);
+          }
+          if (col < p.oscale_cols) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] *= p.oscale;
+          }
+          store4<bf16>(reinterpret_cast<bf16*>(p.out) + (size_t)row * p.ldo + col, v);
+        }
+      }
+  }
+}
+
+
 template <int BM, int BN, int NW, int EPI, int SITE, int KTB = 128, int STAGES = 4, int DIST = 3>
 hipError_t launch_cfg2(const GemmArgs& a, hipStream_t s) {
   if (a.xq < 1 || (a.N / BN) % a.xq) return hipErrorInvalidValue;
@@ -538,10 +731,35 @@ inline int choose_xq(int M, int N, int K, int es, int BN) {
 // position (measured on MI355X at N = 1024, K = 4096: M = 820, 17.5 us against
 // 20.6 us for the best staged tile; M = 1310 ... 1915, 24.4 against 29.3 us);
 // everything else to the register-staged kernel.
+template <int EPI, int SITE>
+hipError_t launch_big(const GemmArgs& a, hipStream_t s) {
+  if (a.xq < 1 || (a.N / 256) % a.xq) return hipErrorInvalidValue;
+  launch((k_gemm_big<EPI, SITE>), dim3((a.N / 256) * ((a.M + 255) / 256)), dim3(512), 0, s, a);
+  return hipGetLastError();
+}
+
+// Where the 256 x 256 kernel wins inside the sampler (kernel traces of the
+// 32^3 workload on MI355X, against the 128 x 128 tiles): the QKV projection
+// (N = 3072, K = 1024) from 8192 rows (32768 rows: 270 -> 231 us; 9831 rows:
+// 90 -> 78 us) and the MLP's second projection (K = 4096) from 16384 rows
+// (343 -> 308 us; at 9831 rows it ties). One 128 KiB workgroup per CU cannot
+// hide its epilogue behind another workgroup's main loop, so the MLP's first
+// projection (GELU, 4096 outputs per row) is slower on it (392 -> 408 us at
+// 32768 rows) and the 1024-wide K = 1024 projections stay on 128 x 128 tiles.
+inline bool use_big(int M, int N, int K) {
+  if (N % 256 || K % 128) return false;
+  if (N == 3 * K) return M >= 8192;
+  return K >= 4096 && M >= 16384;
+}
+
 template <typename T, int EPI, int SITE>
 hipError_t launch_t(const GemmArgs& a0, hipStream_t s) {
   GemmArgs a = a0;
   if constexpr (sizeof(T) == 2) {
+    if (use_big(a.M, a.N, a.K)) {
+      a.xq = choose_xq(a.M, a.N, a.K, 2, 256);
+      return launch_big<EPI, SITE>(a, s);
+    }
     const long rows64 = (a.M + 63) / 64;
     if (a.K >= 4096 && rows64 * (a.N / 64) <= 256) {
       a.xq = choose_xq(a.M, a.N, a.K, 2, 64);

@@ -155,6 +155,75 @@ def test_gemm_bf16_long_k(torch, M, N, K, epi):
     assert np.array_equal(got, got2)
 
 
+def _gemm_big_case(torch, epi, M, N, K, seed, rows=None):
+    """bf16 projection at many rows; the float64 reference on sampled rows."""
+    from paper_2511_22533_amd import f3c
+    rng = np.random.default_rng(seed)
+    A = bf16_round(rng.standard_normal((M, K)).astype(np.float32))
+    W = bf16_round((0.05 * rng.standard_normal((N, K))).astype(np.float32))
+    bias = rng.standard_normal(N).astype(np.float32)
+    gate = rng.standard_normal(N).astype(np.float32)
+    dA, dW, db, dg = to_dev(A, torch.bfloat16), to_dev(W, torch.bfloat16), to_dev(bias), to_dev(gate)
+    say("gemm big", epi, M, N, K)
+    if epi == 2:
+        r0 = rng.standard_normal((M, N)).astype(np.float32)
+        dr = to_dev(r0)
+        f3c.op_gemm(f3c.F3C_BF16, 2, dA, dW, db, resid=dr, gate=dg)
+        torch.cuda.synchronize()
+        got = dr.cpu().numpy()
+        base = r0
+    else:
+        out = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+        f3c.op_gemm(f3c.F3C_BF16, epi, dA, dW, db, out=out)
+        torch.cuda.synchronize()
+        got = out.float().cpu().numpy()
+        base = None
+    if rows is None:
+        rows = np.unique(np.concatenate([rng.choice(M, 384, replace=False), np.arange(M - 130, M)]))
+    ref = A[rows].astype(np.float64) @ W.astype(np.float64).T + bias
+    if epi == 2:
+        return got, (got[rows].astype(np.float64) - base[rows], gate * ref)
+    return got, (got[rows], dit.gelu_tanh(ref) if epi == 1 else ref)
+
+
+# Many rows (the 32^3 workload's active sets) go to the 256 x 256 tiles for the
+# QKV projection shape from 8192 rows and the second MLP projection from 16384
+# (the first MLP projection stays on the smaller tiles): ragged row counts,
+# every epilogue, sampled rows against float64.
+@pytest.mark.parametrize("M,N,K", [(8300, 3072, 1024), (16500, 1024, 4096), (16400, 4096, 1024)])
+@pytest.mark.parametrize("epi", [0, 1, 2])
+def test_gemm_bf16_many_rows(torch, M, N, K, epi):
+    _, (got, want) = _gemm_big_case(torch, epi, M, N, K, seed=M + epi)
+    assert max_rel(got, want) < 1e-2
+
+
+# The tile choice moves with the row count, not the results: the 256 x 256
+# kernel sums K in the same order with the same instruction as the 128 x 128
+# one, so the rows shared by a run just below the switch and one at it agree
+# bit for bit.
+@pytest.mark.parametrize("M,N,K", [(8192, 3072, 1024), (16384, 1024, 4096)])
+@pytest.mark.parametrize("epi", [0, 2])
+def test_gemm_bf16_tile_switch_bit_identical(torch, M, N, K, epi):
+    from paper_2511_22533_amd import f3c
+    rng = np.random.default_rng(M + N + epi)
+    A = to_dev(rng.standard_normal((M, K)).astype(np.float32), torch.bfloat16)
+    W = to_dev((0.05 * rng.standard_normal((N, K))).astype(np.float32), torch.bfloat16)
+    bias = to_dev(rng.standard_normal(N).astype(np.float32))
+    gate = to_dev(rng.standard_normal(N).astype(np.float32))
+    outs = []
+    for rows in (M, M - 1):          # at the switch (256 x 256 tiles), just below it
+        say("gemm tile switch", epi, rows, N, K)
+        if epi == 2:
+            r = torch.zeros((rows, N), dtype=torch.float32, device="cuda")
+            f3c.op_gemm(f3c.F3C_BF16, 2, A[:rows], W, bias, resid=r, gate=gate)
+        else:
+            r = torch.empty((rows, N), dtype=torch.bfloat16, device="cuda")
+            f3c.op_gemm(f3c.F3C_BF16, epi, A[:rows], W, bias, out=r)
+        torch.cuda.synchronize()
+        outs.append(r.float().cpu().numpy())
+    assert np.array_equal(outs[0][:M - 1].view(np.uint32), outs[1].view(np.uint32))
+
+
 @pytest.mark.parametrize("M,N,K", [(1, 128, 32), (300, 384, 128), (513, 512, 128)])
 @pytest.mark.parametrize("epi", [0, 1, 2])
 def test_gemm_f32(torch, M, N, K, epi):
