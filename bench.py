@@ -158,9 +158,10 @@ def hbm_sweep():
       pack_occ      B*V*(4 + 1/8)             (f32 logit per voxel in, one bit out)
       dyn_voxels    B*V/4                     (two packed grids in, Eq. 1)
     Times are per launch with no host gaps (the launches of each size are
-    captured in one graph). The select kernel runs one workgroup per sample
-    (keys stay in LDS), so it cannot fill the chip below about 256 samples:
-    its figures are latency."""
+    captured in one graph). A selection call is two kernels: the scoring pass
+    streams the caches over the whole chip (its share: B*N*64 bytes), then one
+    workgroup per sample selects from its keys held in LDS, so below about
+    256 samples that second kernel's time is latency."""
     import torch
     from paper_2511_22533_amd import f3c, synth
     torch.cuda.set_device(0)
