@@ -102,7 +102,12 @@ int f3c_weight_info(const f3c_model* m, int32_t i, const char** name, int64_t* n
 int f3c_model_weights_bytes(const f3c_model* m, size_t* bytes);
 
 /* Bind a caller-allocated device buffer (>= f3c_model_weights_bytes) and upload
- * the parameters from host float32 arrays given in canonical order. Matrices are
+ * the parameters of the transformer of Sec. 3.2 (per block: the modulation,
+ * attention, cross-attention and MLP weights that the supplement's FLOPs list
+ * counts) from host float32 arrays given in canonical order
+ * (f3c_weight_info names them). Errors: F3C_EINVAL (NULL arrays, a count that
+ * differs from the model's, a buffer not 256-byte aligned), F3C_ENOMEM (buffer
+ * too small), F3C_EHIP (copy). Matrices are
  * rounded to the model dtype (round-to-nearest-even for bf16); biases stay f32.
  * Synchronous: returns after the upload completed. */
 int f3c_model_load_weights(f3c_model* m, void* weights_dev, size_t bytes, const float* const* host_f32,
@@ -142,8 +147,11 @@ int f3c_state_reset(f3c_state* s, f3c_stream stream);
 int f3c_state_set_omega(f3c_state* s, float omega);
 
 /* Precompute the cross-attention keys/values of every block from the condition
- * tokens cond_dev (float32 [B][Nc][dc], device). They depend only on the
- * condition and the weights, so one call serves the whole trajectory. */
+ * tokens cond_dev (float32 [B][Nc][dc], device): the image conditioning of the
+ * flow transformer (Sec. 3.2; the "Cross Attention" term of the supplement's
+ * FLOPs list projects Nc condition tokens of width dc per block). They depend
+ * only on the condition and the weights, so one call serves the whole
+ * trajectory. Errors: F3C_EINVAL (NULL pointer). */
 int f3c_set_cond(f3c_state* s, const float* cond_dev, f3c_stream stream);
 
 /* The unconditional input of classifier-free guidance (float32 [B][Nc][dc],
@@ -256,9 +264,11 @@ int f3c_state_trace_sublayers(f3c_state* s, float* sub_trace_dev, size_t bytes);
  * NULL disarms. Errors: F3C_EINVAL (NULL state, misaligned buffer). */
 int f3c_debug_force_active(f3c_state* s, const int32_t* idx_active_dev);
 
-/* Checkpoint: the sampler state beyond x is the cache pair. export copies
- * v_cache then v_prev (2*B*N*8 floats) to host memory; import restores them.
- * Both synchronise `stream`. */
+/* Checkpoint: what Algorithm 1 carries from one step to the next besides the
+ * latent x_t is the velocity cache pair (v_cache, v_prev_cache). export copies
+ * v_cache then v_prev (2*B*N*8 floats, host memory owned by the caller) to
+ * host; import restores them. Both synchronise `stream`. Errors: F3C_EINVAL
+ * (NULL pointers), F3C_ENOMEM (n_floats below 2*B*N*8), F3C_EHIP (copy). */
 int f3c_state_export(const f3c_state* s, float* host, size_t n_floats, f3c_stream stream);
 int f3c_state_import(f3c_state* s, const float* host, size_t n_floats, f3c_stream stream);
 
