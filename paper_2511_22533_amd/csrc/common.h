@@ -74,10 +74,17 @@ template <typename T> __device__ __forceinline__ T from_f32(float x);
 template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
 template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return static_cast<bf16>(x); }
 
+// GELU in its tanh form, 0.5 x (1 + tanh(u)) with u = sqrt(2/pi) (x + 0.044715 x^3),
+// evaluated as the identical x / (1 + e^(-2u)): one exponential and one
+// reciprocal instead of the library tanhf (measured on MI355X: the MLP's first
+// projection at 32768 rows, 485 -> 447 us; a plain store takes 440 us). For
+// u far below zero e^(-2u) overflows to +inf and the result is -0.
 __device__ __forceinline__ float gelu_tanh(float x) {
   const float k0 = 0.7978845608028654f;   // sqrt(2/pi)
   const float k1 = 0.044715f;
-  return 0.5f * x * (1.0f + tanhf(k0 * (x + k1 * x * x * x)));
+  const float u = k0 * (x + k1 * x * x * x);
+  const float e = __builtin_amdgcn_exp2f(u * -2.8853900817779268f);   // 2^(-2u log2(e)) = e^(-2u)
+  return x * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
 __device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
