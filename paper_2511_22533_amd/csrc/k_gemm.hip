@@ -738,28 +738,31 @@ hipError_t launch_big(const GemmArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Where the 256 x 256 kernel wins inside the sampler (kernel traces of the
-// 32^3 workload on MI355X, against the 128 x 128 tiles): the QKV projection
-// (N = 3072, K = 1024) from 8192 rows (32768 rows: 270 -> 231 us; 9831 rows:
-// 90 -> 78 us) and the MLP's second projection (K = 4096) from 8192 rows when
-// each XCD takes whole row panels (below). One 128 KiB workgroup per CU cannot
-// hide its epilogue behind another workgroup's main loop, so the MLP's first
-// projection (GELU, 4096 outputs per row) is slower on it (392 -> 408 us at
-// 32768 rows) and the 1024-wide K = 1024 projections stay on 128 x 128 tiles.
+// Where the 256 x 256 kernel wins inside the sampler (MI355X, against the
+// 128 x 128 tiles): from 8192 rows, the QKV projection (N = 3K; 32768 rows:
+// 270 -> 231 us, 9831 rows: 90 -> 78 us in the sampler's traces), the MLP's
+// first projection (N = 4K, GELU; 32768 rows: 451-457 -> 386 us, 9831 rows:
+// 127-129 -> 121 us) and its second (K = 4096; 339 against 418-437 us at 32768
+// rows). The 1024-wide K = 1024 projections stay on 128 x 128 tiles (a tie at
+// 32768 rows, 50 against 45 us at 9831): one 128 KiB workgroup per CU cannot
+// hide its residual epilogue behind another workgroup's main loop.
 inline bool use_big(int M, int N, int K) {
-  if (N % 256 || K % 128) return false;
-  if (N == 3 * K) return M >= 8192;
-  return K >= 4096 && M >= 8192;
+  if (N % 256 || K % 128 || M < 8192) return false;
+  return N == 3 * K || N == 4 * K || K >= 4096;
 }
 
 // Column groups of the 256 x 256 kernel. With K = 4096 the weight (8 MiB at
 // N = 1024) cannot stay in an XCD's L2 whatever the grouping, while the four
 // column tiles of a row panel run side by side on one XCD and share its
-// 2 MiB A panel; so each XCD takes whole row panels (xq = 1: A read once).
-// Measured on MI355X at N = 1024, K = 4096: 32768 rows 339 us against 363 us
-// at xq = 4 (the L2-fit rule's pick), 9831 rows 116 against 119-121 us (the
-// 128 x 128 tiles: 120-125 us).
-inline int big_xq(int M, int N, int K) { return K >= 4096 ? 1 : choose_xq(M, N, K, 2, 256); }
+// 2 MiB A panel; so each XCD takes whole row panels (xq = 1: A read once;
+// 32768 rows 339 us against 363 us at xq = 4, the L2-fit rule's pick). The
+// GELU projection (N = 4K) measured best at two column groups (32768 rows:
+// 386 against 407-410 us at xq = 4; 9831 rows: 121 against 125-128 us).
+inline int big_xq(int M, int N, int K) {
+  if (K >= 4096) return 1;
+  if (N == 4 * K && (N / 256) % 2 == 0) return 2;
+  return choose_xq(M, N, K, 2, 256);
+}
 
 template <typename T, int EPI, int SITE>
 hipError_t launch_t(const GemmArgs& a0, hipStream_t s) {

@@ -187,11 +187,10 @@ def _gemm_big_case(torch, epi, M, N, K, seed, rows=None):
 
 
 # Many rows (the 32^3 workload's active sets) go to the 256 x 256 tiles for the
-# QKV projection shape and the second MLP projection from 8192 rows (the first
-# MLP projection stays on the smaller tiles): ragged row counts, every
-# epilogue, sampled rows against float64.
+# QKV projection shape and both MLP projections from 8192 rows: ragged row
+# counts, every epilogue, sampled rows against float64.
 @pytest.mark.parametrize("M,N,K", [(8300, 3072, 1024), (9831, 1024, 4096), (16500, 1024, 4096),
-                                   (16400, 4096, 1024)])
+                                   (9831, 4096, 1024), (16400, 4096, 1024)])
 @pytest.mark.parametrize("epi", [0, 1, 2])
 def test_gemm_bf16_many_rows(torch, M, N, K, epi):
     _, (got, want) = _gemm_big_case(torch, epi, M, N, K, seed=M + epi)
@@ -202,7 +201,7 @@ def test_gemm_bf16_many_rows(torch, M, N, K, epi):
 # kernel sums K in the same order with the same instruction as the 128 x 128
 # one, so the rows shared by a run just below the switch and one at it agree
 # bit for bit.
-@pytest.mark.parametrize("M,N,K", [(8192, 3072, 1024), (8192, 1024, 4096)])
+@pytest.mark.parametrize("M,N,K", [(8192, 3072, 1024), (8192, 1024, 4096), (8192, 4096, 1024)])
 @pytest.mark.parametrize("epi", [0, 2])
 def test_gemm_bf16_tile_switch_bit_identical(torch, M, N, K, epi):
     from paper_2511_22533_amd import f3c
