@@ -314,6 +314,16 @@ int f3c_profile_reset(f3c_state* s);
  * F3C_EINVAL (shapes, NULL or misaligned buffers, omega outside [0, 1]),
  * F3C_ENOMEM (workspace too small). */
 int f3c_op_select_workspace_bytes(int32_t batch, int32_t n_tokens, size_t* bytes);
+/* The selection step alone (Algorithm 1, SSC: the n_cache_host[b] tokens of
+ * lowest score are cached, ties to the lower token index, NaN after every
+ * number; Sec. 4.2: the active set as ascending token indices) from
+ * caller-given scores, float32 [B][N] on the device, e.g. another
+ * implementation's scores: a parity hook for the selection independent of
+ * the scoring arithmetic. Writes idx_active and pos as f3c_op_select does;
+ * needs no workspace. Errors: F3C_EINVAL (shapes, NULL pointers,
+ * n_cache_host[b] outside [0, N]). */
+int f3c_op_select_scores(int32_t batch, int32_t n_tokens, const float* scores, const int32_t* n_cache_host,
+                         int32_t* idx_active, int32_t* pos, f3c_stream stream);
 int f3c_op_select(int32_t batch, int32_t n_tokens, const float* v_cache, const float* v_prev, float omega,
                   const int32_t* n_cache_host, int32_t* idx_active, int32_t* pos, float* score, void* workspace,
                   size_t workspace_bytes, f3c_stream stream);

@@ -155,10 +155,13 @@ __global__ __launch_bounds__(kStatThreads) void k_score_stats(const float* __res
   }
 }
 
+// FROM_SCORES: the keys come from caller-given scores (given [B][N]) instead
+// of the magnitude pairs; everything after the keys is the same.
+template <bool FROM_SCORES>
 __global__ __launch_bounds__(kThreads) void k_select(const float2* __restrict__ va, const float4* __restrict__ partial,
                                                      int chunks, int N, float w_a, float w_v, Segs n_cache, Segs act,
                                                      int32_t* __restrict__ idx_active, int32_t* __restrict__ pos,
-                                                     float* __restrict__ score) {
+                                                     float* __restrict__ score, const float* __restrict__ given) {
   __shared__ uint32_t keys[kMaxTokens];
   __shared__ int hist[256];
   __shared__ int cnt_eq[kMaxTokens / 64], cnt_act[kMaxTokens / 64];   // per (round, wave)
@@ -180,27 +183,32 @@ __global__ __launch_bounds__(kThreads) void k_select(const float2* __restrict__ 
     return;
   }
 
-  // The sample's extremes from the partials (chunks <= 64: one wave).
-  if (wave == 0) {
-    float4 m = lane < chunks ? partial[(size_t)b * chunks + lane] : make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY);
+  if constexpr (FROM_SCORES) {
+    for (int i = tid; i < N; i += kThreads) keys[i] = order_key(given[base + i]);
+  } else {
+    // The sample's extremes from the partials (chunks <= 64: one wave).
+    if (wave == 0) {
+      float4 m = lane < chunks ? partial[(size_t)b * chunks + lane]
+                               : make_float4(INFINITY, -INFINITY, INFINITY, -INFINITY);
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      m.x = fminf(m.x, __shfl_xor(m.x, o));
-      m.y = fmaxf(m.y, __shfl_xor(m.y, o));
-      m.z = fminf(m.z, __shfl_xor(m.z, o));
-      m.w = fmaxf(m.w, __shfl_xor(m.w, o));
+      for (int o = 32; o > 0; o >>= 1) {
+        m.x = fminf(m.x, __shfl_xor(m.x, o));
+        m.y = fmaxf(m.y, __shfl_xor(m.y, o));
+        m.z = fminf(m.z, __shfl_xor(m.z, o));
+        m.w = fmaxf(m.w, __shfl_xor(m.w, o));
+      }
+      if (lane == 0) ext = m;
     }
-    if (lane == 0) ext = m;
-  }
-  __syncthreads();
-  const float loV = ext.x, hiV = ext.y, loA = ext.z, hiA = ext.w;
+    __syncthreads();
+    const float loV = ext.x, hiV = ext.y, loA = ext.z, hiA = ext.w;
 
-  // Scores and order keys.
-  for (int i = tid; i < N; i += kThreads) {
-    const float2 p = va[base + i];
-    const float cs = __fadd_rn(__fmul_rn(w_a, norm_term(p.y, loA, hiA)), __fmul_rn(w_v, norm_term(p.x, loV, hiV)));
-    keys[i] = order_key(cs);
-    if (score) score[base + i] = cs;
+    // Scores and order keys.
+    for (int i = tid; i < N; i += kThreads) {
+      const float2 p = va[base + i];
+      const float cs = __fadd_rn(__fmul_rn(w_a, norm_term(p.y, loA, hiA)), __fmul_rn(w_v, norm_term(p.x, loV, hiV)));
+      keys[i] = order_key(cs);
+      if (score) score[base + i] = cs;
+    }
   }
   __syncthreads();
 
@@ -375,8 +383,15 @@ hipError_t launch_select(const float* v_cache, const float* v_prev, int B, int N
   float4* partial = reinterpret_cast<float4*>(static_cast<char*>(workspace) +
                                               (((size_t)B * N * sizeof(float2) + 255) & ~(size_t)255));
   launch(k_score_stats, dim3(chunks, B), dim3(kStatThreads), 0, s, v_cache, v_prev, N, n_cache, va, partial, chunks);
-  launch(k_select, dim3(B), dim3(kThreads), 0, s, (const float2*)va, (const float4*)partial, chunks, N, w_a, w_v,
-         n_cache, act, idx_active, pos, score);
+  launch(k_select<false>, dim3(B), dim3(kThreads), 0, s, (const float2*)va, (const float4*)partial, chunks, N, w_a,
+         w_v, n_cache, act, idx_active, pos, score, (const float*)nullptr);
+  return hipGetLastError();
+}
+
+hipError_t launch_select_scores(const float* scores, int B, int N, const Segs& n_cache, const Segs& act,
+                                int32_t* idx_active, int32_t* pos, hipStream_t s) {
+  launch(k_select<true>, dim3(B), dim3(kThreads), 0, s, (const float2*)nullptr, (const float4*)nullptr, 0, N, 0.0f,
+         0.0f, n_cache, act, idx_active, pos, (float*)nullptr, scores);
   return hipGetLastError();
 }
 

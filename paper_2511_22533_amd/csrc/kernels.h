@@ -36,6 +36,10 @@ size_t select_workspace_bytes(int B, int N);
 hipError_t launch_select(const float* v_cache, const float* v_prev, int B, int N, float w_a, float w_v,
                          const Segs& n_cache, const Segs& act, int32_t* idx_active, int32_t* pos,
                          float* score, void* workspace, hipStream_t s);
+// The selection alone from caller-given float32 scores [B][N] (the same keys,
+// radix select and token-order scan; no workspace).
+hipError_t launch_select_scores(const float* scores, int B, int N, const Segs& n_cache, const Segs& act,
+                                int32_t* idx_active, int32_t* pos, hipStream_t s);
 // Device address and size of the selection's static scratch on the current
 // device (looked up once per device, then cached).
 hipError_t select_static_scratch(void** ptr, size_t* bytes);

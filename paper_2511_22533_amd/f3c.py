@@ -82,6 +82,7 @@ _SIGS = {
     "f3c_op_select": (c_int, [c_int, c_int, c_p, c_p, c_f, P_i32, c_p, c_p, c_p, c_p, c_sz, c_p]),
     "f3c_op_select_workspace_bytes": (c_int, [c_int, c_int, ctypes.POINTER(c_sz)]),
     "f3c_op_select_noalloc": (c_int, [c_int, c_int, c_p, c_p, c_f, P_i32, c_p, c_p, c_p, c_p]),
+    "f3c_op_select_scores": (c_int, [c_int, c_int, c_p, P_i32, c_p, c_p, c_p]),
     "f3c_op_gemm": (c_int, [c_int, c_int, c_int, c_int, c_int, c_p, c_int, c_p, c_int, c_p, c_p, c_p, c_int, c_p,
                             c_int, c_p]),
     "f3c_op_attention": (c_int, [c_int, c_int, c_int, c_int, P_i32, P_i32, c_p, c_int, c_p, c_int, c_p, c_int, c_p,
@@ -448,6 +449,13 @@ def op_select_noalloc(v_cache, v_prev, omega: float, n_cache: Sequence[int], idx
     B, N = v_cache.shape[0], v_cache.shape[1]
     check(lib().f3c_op_select_noalloc(B, N, v_cache.data_ptr(), v_prev.data_ptr(), omega, _i32(n_cache),
                                       idx_active.data_ptr(), pos.data_ptr(), _ptr(score), _stream(stream)))
+
+
+def op_select_scores(scores, n_cache: Sequence[int], idx_active, pos, stream=None):
+    """The selection alone from given float32 scores [B][N] (device)."""
+    B, N = scores.shape[0], scores.shape[1]
+    check(lib().f3c_op_select_scores(B, N, scores.data_ptr(), _i32(n_cache), idx_active.data_ptr(), pos.data_ptr(),
+                                     _stream(stream)))
 
 
 def op_gemm(dtype: int, epilogue: int, A, W, bias, out=None, resid=None, gate=None, stream=None):

@@ -136,6 +136,13 @@ def test_op_entry_validation_is_host_side(L):
     assert L.f3c_op_select(1, 512, 1, 1, 0.7, q, 1, 1, None, None, 1 << 20, None) == f3c.F3C_EINVAL
     assert L.f3c_op_select(1, 512, 1, 1, 0.7, q, 1, 1, None, 128, 1 << 20, None) == f3c.F3C_EINVAL
     assert L.f3c_op_select(1, 512, 1, 1, 0.7, q, 1, 1, None, 256, 64, None) == f3c.F3C_ENOMEM
+    # selection from given scores: NULL scores, quota outside [0, N], bad shapes
+    assert L.f3c_op_select_scores(1, 512, None, q, 1, 1, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_select_scores(1, 4, 1, f3c._i32([5]), 1, 1, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_select_scores(1, 4, 1, f3c._i32([-1]), 1, 1, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_select_scores(65, 4, 1, f3c._i32([0] * 65), 1, 1, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_select_scores(1, 40000, 1, f3c._i32([5]), 1, 1, None) == f3c.F3C_EINVAL
+    assert L.f3c_op_select_scores(1, 512, 1, q, None, 1, None) == f3c.F3C_EINVAL
     assert f3c.select_workspace_bytes(1, 512) == 512 * 8 + 16
     assert f3c.select_workspace_bytes(4, 32768) == 4 * 32768 * 8 + 4 * 32 * 16
     assert L.f3c_op_gemm(1, 0, 16, 100, 64, 1, 64, 1, 64, 1, None, 1, 100, None, 0, None) == f3c.F3C_EINVAL

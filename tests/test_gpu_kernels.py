@@ -98,6 +98,45 @@ def test_select_degenerate_and_nan(torch):
     _check_select(torch, vc, vp, [100, 1500, 2047])
 
 
+# The selection alone from given scores (f3c_op_select_scores) against the
+# oracle's stable sort of the same scores: ragged quotas including 0, 1, N - 1
+# and N; heavy ties (a few distinct values), NaN, +-inf, +-0 and subnormals.
+@pytest.mark.parametrize("B,N", [(1, 1), (3, 1000), (4, 4096), (2, 32768)])
+def test_select_from_given_scores(torch, B, N):
+    from paper_2511_22533_amd import f3c
+    rng = np.random.default_rng(7 * N + B)
+    cases = {
+        "continuous": rng.standard_normal((B, N)).astype(np.float32),
+        "ties": (rng.integers(0, 5, size=(B, N)) * 0.25).astype(np.float32),
+    }
+    special = rng.random((B, N)).astype(np.float32)
+    picks = rng.integers(0, N, size=(B, 6 * max(1, N // 64)))
+    for b in range(B):
+        for j, i in enumerate(picks[b]):
+            special[b, i] = [np.nan, np.inf, -np.inf, 0.0, -0.0, np.float32(1e-45)][j % 6]
+    cases["special"] = special
+    for name, sc in cases.items():
+        quota_sets = [[0] * B, [N] * B, [min(1, N)] * B, [max(N - 1, 0)] * B,
+                      [int(q) for q in rng.integers(0, N + 1, size=B)]]
+        for quotas in quota_sets:
+            say("select scores", name, B, N, quotas)
+            tot = sum(N - c for c in quotas)
+            idx = torch.full((max(tot, 1),), -7, dtype=torch.int32, device="cuda")
+            pos = torch.full((B, N), -7, dtype=torch.int32, device="cuda")
+            f3c.op_select_scores(to_dev(sc), quotas, idx, pos)
+            torch.cuda.synchronize()
+            got_idx, got_pos = idx.cpu().numpy(), pos.cpu().numpy()
+            row = 0
+            for b in range(B):
+                _, active = ssc.select(sc[b], quotas[b])
+                n = len(active)
+                assert np.array_equal(got_idx[row:row + n], active), (name, quotas, b)
+                want_pos = np.full(N, -1, np.int64)
+                want_pos[active] = row + np.arange(n)
+                assert np.array_equal(got_pos[b], want_pos), (name, quotas, b)
+                row += n
+
+
 def _gemm_case(torch, dt, epi, M, N, K, seed):
     from paper_2511_22533_amd import f3c
     rng = np.random.default_rng(seed)
