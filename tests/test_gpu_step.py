@@ -139,8 +139,9 @@ def test_tiny_f32_amplified_sublayers(torch):
     cfg = synth.TINY
     pair = Pair(cfg, 2, seed=5, scale=0.08)
     x = to_dev(pair.x_T)
-    times = schedule.time_grid(6, 1.0)
-    for k, q in enumerate([[0, 0], [0, 0], [100, 300], [256, 0], [511, 1], [512, 200]]):
+    times = schedule.time_grid(7, 1.0)
+    # the last two steps: one sample's active set empty, then every sample's (no transformer rows at all)
+    for k, q in enumerate([[0, 0], [0, 0], [100, 300], [256, 0], [511, 1], [512, 200], [512, 512]]):
         say("tiny amplified step", k + 1, q)
         r = _gpu_step(torch, pair, x, times[k], times[k + 1], q)
         _check_step(pair, r, times[k], times[k + 1], q, 1e-4)
