@@ -946,7 +946,7 @@ int f3c_op_select(int32_t batch, int32_t n_tokens, const float* v_cache, const f
 int f3c_op_select_scores(int32_t batch, int32_t n_tokens, const float* scores, const int32_t* n_cache_host,
                          int32_t* idx_active, int32_t* pos, f3c_stream stream) {
   Segs quota, act;
-  if (!scores) return fail(F3C_EINVAL, "NULL argument");
+  // the same shape and quota checks as f3c_op_select, with the scores in place of the two caches
   if (int rc = select_args(batch, n_tokens, scores, scores, 0.0f, n_cache_host, idx_active, pos, &quota, &act))
     return rc;
   HIP_TRY(launch_select_scores(scores, batch, n_tokens, quota, act, idx_active, pos, (hipStream_t)stream));
