@@ -25,8 +25,10 @@ here comes from the HIP library. One file per workload and sample,
 A batch-4 workload's samples are independent trajectories (each has its own
 noise, condition and quota column), so each is written from a batch-1 run.
 
-The oracle takes minutes per step at these sizes; ``--checkpoint DIR`` keeps
-the state after every step there, and a rerun resumes from it.
+The oracle takes minutes per step at these sizes (about 40 minutes per full
+step of the 32^3 model); ``--checkpoint DIR`` keeps the sampler state after
+every step there and the residual stream after every transformer block of the
+step in progress, and a rerun resumes from the last of them.
 
 Usage (repository root):
     python tests/golden/make_trajectories.py --workload trellis16_cached
@@ -70,10 +72,40 @@ def sample_inputs(workload: str, sample: int):
     return w, cfg, W, x_T, cond, quotas, times
 
 
+def resumable_velocity(model: dit.Model, cond: np.ndarray, path: str | None):
+    """The velocity of oracle.sampler.model_velocity, with the residual stream
+    kept at ``path`` after every block: the same calls of the oracle in the
+    same order as dit.Model.forward (modulation, embedding, the blocks, the
+    final norm and projection), so a resumed step returns the same array."""
+    if path is None:
+        return sampler.model_velocity(model, cond)
+
+    def fn(b, x_active, idx, t):
+        mod = model.modulation(t)
+        tag = np.array([float(t), float(b), float(idx.size), float(np.sum(idx, dtype=np.int64))])
+        l0, h = 0, None
+        if os.path.exists(path):
+            with np.load(path) as z:
+                if np.array_equal(z["tag"], tag) and np.array_equal(z["idx"], idx):
+                    l0, h = int(z["blocks_done"]), z["h"].copy()
+                    print(f"[golden]   resuming the step after block {l0}", flush=True)
+        if h is None:
+            h = model.embed(x_active, idx)
+        for l in range(l0, model.cfg.depth):
+            ck, cv = model.cond_kv(cond[b], l)
+            h = model.block(l, h, mod[l], ck, cv)
+            tmp = path + ".tmp.npz"
+            np.savez(tmp, tag=tag, idx=idx, blocks_done=np.int64(l + 1), h=h)
+            os.replace(tmp, path)
+        return dit.linear(dit.layer_norm(h), model.w["out_w"], model.w["out_b"])
+    return fn
+
+
 def run(workload: str, sample: int, checkpoint: str | None) -> str:
     w, cfg, W, x_T, cond, quotas, times = sample_inputs(workload, sample)
     T, N = w.steps, cfg.tokens
-    velocity = sampler.model_velocity(dit.Model(cfg, W), cond)
+    bpath = os.path.join(checkpoint, f"{workload}.s{sample}.block.npz") if checkpoint else None
+    velocity = resumable_velocity(dit.Model(cfg, W), cond, bpath)
     st = sampler.State.start(x_T)
     out = {"quotas": quotas, "times": times, "active": np.zeros((T, N // 8), np.uint8)}
     k0 = 0
