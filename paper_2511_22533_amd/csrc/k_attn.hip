@@ -403,6 +403,9 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
 #pragma unroll
         for (int q = 0; q < NKS; ++q)
           kf[kt][q] = *reinterpret_cast<const u32x4*>(Ks + (kt * 32 + r32) * KRS + (((2 * q + g) ^ kswz) << 4));
+      // All eight reads go out before the first MFMA (left to itself the
+      // scheduler pairs each read with its MFMAs, one LDS latency per pair).
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int q = 0; q < NKS; ++q)
 #pragma unroll
@@ -412,9 +415,12 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
     };
     // O^T += V^T P^T for the tile in buffer buf; keys kb..kb+3 and kb+8..kb+11
     // at column h*32 + (lane%32) through two transpose reads of the row-major
-    // V tile (the K-slot order of P).
+    // V tile (the K-slot order of P). As for the scores, every fragment read
+    // is issued before the first MFMA (2-3% faster at 9831 and 32768 tokens
+    // than the scheduler's read-per-MFMA order; same instructions and results).
     auto pv2 = [&](int buf, const bf16x8 (&pf)[2][2]) {
       const char* Vt = lds + buf * SB + kgrp * TB + KBUF;
+      bf16x8 vfs[2][2][HT];
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
@@ -425,9 +431,15 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
             const char* a0 = Vt + (kb + vrow) * (HD * ES) + (((col >> 3) ^ vswz) << 4) + (col & 7) * ES;
             const auto lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)a0);
             const auto hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(a0 + 8 * HD * ES));
-            const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-            oacc[h] = Mfma<T>::mma(vf, pf[kt][u], oacc[h]);
+            vfs[kt][u][h] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
           }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int h = 0; h < HT; ++h) oacc[h] = Mfma<T>::mma(vfs[kt][u][h], pf[kt][u], oacc[h]);
     };
     // Keys of element e: kv0 + 32*kt + 8*(e/4) + 4*g + e%4; mask those past nk.
     auto mask2 = [&](int t, f32x16 (&s)[2]) {
