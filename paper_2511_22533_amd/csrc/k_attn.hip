@@ -225,18 +225,26 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
   //      take 32 bytes from each of 4 consecutive rows)
   constexpr int DBLK = kBKV / 8;                       // 8-row blocks per tile
   constexpr int DQ = (DBLK + NW - 1) / NW;             // blocks per wave
+  // DMA addresses: scalar bases (this sample's first key row of this head) and
+  // 32-bit lane offsets, the same for every tile but for the key index (the
+  // host checks that nk rows of either operand stay below 2 GiB); M0 from
+  // wave-uniform values. Four vector instructions per tile instead of ten.
+  const char* kbase = p.k + ((size_t)k_begin * p.ldk + head * HD) * ES;
+  const char* vbase = p.v + ((size_t)k_begin * p.ldv + head * HD) * ES;
+  const uint32_t ldk_b = (uint32_t)p.ldk * ES, ldv_b = (uint32_t)p.ldv * ES;
+  const uint32_t lds_u = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   auto fetch_dma = [&](int kv0, int stage, int k) {
-    char* Ks = lds + stage * SB + k * TB;
-    char* Vs = Ks + KBUF;
 #pragma unroll
     for (int q = 0; q < DQ; ++q) {
-      const int blk = min(wave + NW * q, DBLK - 1);
-      const int row = blk * 8 + (lane >> 3), phys = lane & 7;
-      const int key = min(kv0 + row, nk - 1);
-      const size_t kofs = ((size_t)(k_begin + key) * p.ldk + head * HD) * ES;
-      const size_t vofs = ((size_t)(k_begin + key) * p.ldv + head * HD) * ES;
-      dma16(p.k + kofs + ((phys ^ ((row >> 1) & 7)) << 4), Ks + blk * 1024);
-      dma16(p.v + vofs + ((phys ^ (((row >> 1) & 1) << 2)) << 4), Vs + blk * 1024);
+      const int blk_u = min(wave_u + NW * q, DBLK - 1);
+      const int row = blk_u * 8 + (lane >> 3), phys = lane & 7;
+      const uint32_t key = (uint32_t)min(kv0 + row, nk - 1);
+      const uint32_t kofs = key * ldk_b + (uint32_t)((phys ^ ((row >> 1) & 7)) << 4);
+      const uint32_t vofs = key * ldv_b + (uint32_t)((phys ^ (((row >> 1) & 1) << 2)) << 4);
+      const uint32_t kl = lds_u + (uint32_t)(stage * SB + k * TB + blk_u * 1024);
+      asm volatile("global_load_lds_dwordx4 %0, %1" : : "v"(kofs), "s"(kbase), "{m0}"(kl) : "memory");
+      asm volatile("global_load_lds_dwordx4 %0, %1" : : "v"(vofs), "s"(vbase), "{m0}"(kl + (uint32_t)KBUF) : "memory");
     }
   };
 
@@ -467,7 +475,14 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
           for (int e = 0; e < 8; ++e)
             pf[kt][u][e] = (bf16)__builtin_amdgcn_exp2f(QS ? s[kt][8 * u + e] : s[kt][8 * u + e] * c);
           const bf16x8& f = pf[kt][u];
-          float a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(f, f, 0, 1), ones, 0.0f, false);
+          // the chain's first dot in the three-operand form with a zero
+          // accumulator (no register to clear first); the nop covers a dot
+          // result read by the next dot as its accumulator
+          float a;
+          {
+            const bf16x2 f01 = __builtin_shufflevector(f, f, 0, 1);
+            asm("v_dot2_f32_bf16 %0, %1, %2, 0\n\ts_nop 1" : "=v"(a) : "v"(f01), "v"(ones));
+          }
           a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(f, f, 2, 3), ones, a, false);
           a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(f, f, 4, 5), ones, a, false);
           part[2 * kt + u] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(f, f, 6, 7), ones, a, false);
@@ -794,6 +809,10 @@ hipError_t launch_site(int dt, int hd, const AttnArgs& a, int heads, float* ws, 
     kt_min = std::min(kt_min, kt);
     kt_max = std::max(kt_max, kt);
   }
+  // The DMA path addresses a sample's key and value rows with 32-bit offsets
+  // from the sample's first row.
+  if (dt == DT_BF16 && hd == 64 && kt_max * kBKV * (int64_t)std::max(a.ldk, a.ldv) * 2 >= (int64_t(1) << 31))
+    return hipErrorInvalidValue;
   if (t256 * heads >= 160) return launch_a<8, SITE>(dt, hd, a, heads, 1, s, qs);
   int splits = 1;
   while (splits < 8 && t128 * heads * splits * 2 <= 256 && kt_min >= 16 * splits) splits *= 2;
