@@ -137,6 +137,9 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
   constexpr int VPR = (VITEMS + NT - 1) / NT;
   constexpr int KBUF = kBKV * KRS, VBUF = DMA ? kBKV * HD * ES : HD * VRS;
   constexpr int TB = KBUF + VBUF, SB = KS * TB;      // bytes per tile, per stage
+  // DMA path: the K tiles of all stages, then the V tiles (VREG on), so that a
+  // fragment read's stage offset fits the 16-bit offset field of the LDS read.
+  constexpr int VREG = NBUF * KS * KBUF;
   __shared__ __attribute__((aligned(16))) char lds[NBUF * SB];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -242,9 +245,10 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
       const uint32_t key = (uint32_t)min(kv0 + row, nk - 1);
       const uint32_t kofs = key * ldk_b + (uint32_t)((phys ^ ((row >> 1) & 7)) << 4);
       const uint32_t vofs = key * ldv_b + (uint32_t)((phys ^ (((row >> 1) & 1) << 2)) << 4);
-      const uint32_t kl = lds_u + (uint32_t)(stage * SB + k * TB + blk_u * 1024);
+      const uint32_t kl = lds_u + (uint32_t)((stage * KS + k) * KBUF + blk_u * 1024);
+      const uint32_t vl = lds_u + (uint32_t)(VREG + (stage * KS + k) * VBUF + blk_u * 1024);
       asm volatile("global_load_lds_dwordx4 %0, %1" : : "v"(kofs), "s"(kbase), "{m0}"(kl) : "memory");
-      asm volatile("global_load_lds_dwordx4 %0, %1" : : "v"(vofs), "s"(vbase), "{m0}"(kl + (uint32_t)KBUF) : "memory");
+      asm volatile("global_load_lds_dwordx4 %0, %1" : : "v"(vofs), "s"(vbase), "{m0}"(vl) : "memory");
     }
   };
 
@@ -404,7 +408,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) minit[e] = 0.0f;
     auto qk2 = [&](int buf, f32x16 (&s)[2]) {
-      const char* Ks = lds + buf * SB + kgrp * TB;
+      const char* Ks = lds + (buf * KS + kgrp) * KBUF;
       u32x4 kf[2][NKS];
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
@@ -427,7 +431,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
     // is issued before the first MFMA (2-3% faster at 9831 and 32768 tokens
     // than the scheduler's read-per-MFMA order; same instructions and results).
     auto pv2 = [&](int buf, const bf16x8 (&pf)[2][2]) {
-      const char* Vt = lds + buf * SB + kgrp * TB + KBUF;
+      const char* Vt = lds + VREG + (buf * KS + kgrp) * VBUF;
       bf16x8 vfs[2][2][HT];
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
@@ -586,6 +590,21 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
       } else {
         mid(0, 0, sa, sb, pb, pa, yes);                // S(1) in sb, P(0) in pa
         int i = 1, buf = 1;
+        if constexpr (NBUF == 5) {
+          // ten steps per round with literal stages: their offsets fold into the reads
+          for (; i + 10 < n_steps; i += 10) {
+            mid(i, 1, sb, sa, pa, pb, no);
+            mid(i + 1, 2, sa, sb, pb, pa, no);
+            mid(i + 2, 3, sb, sa, pa, pb, no);
+            mid(i + 3, 4, sa, sb, pb, pa, no);
+            mid(i + 4, 0, sb, sa, pa, pb, no);
+            mid(i + 5, 1, sa, sb, pb, pa, no);
+            mid(i + 6, 2, sb, sa, pa, pb, no);
+            mid(i + 7, 3, sa, sb, pb, pa, no);
+            mid(i + 8, 4, sb, sa, pa, pb, no);
+            mid(i + 9, 0, sa, sb, pb, pa, no);
+          }
+        }
         for (; i + 2 < n_steps; i += 2, buf = bnext(buf, 2)) {
           mid(i, buf, sb, sa, pa, pb, no);
           mid(i + 1, bnext(buf, 1), sa, sb, pb, pa, no);
