@@ -370,7 +370,11 @@ int f3c_op_gemm(int32_t dtype, int32_t epilogue, int32_t M, int32_t N, int32_t K
  * each split's unnormalised output, max and sum go to the workspace (splits *
  * rows * heads * (head_dim + 2) floats) and are merged in split order, so
  * results do not depend on scheduling. The split count shrinks to what the
- * workspace holds; without a workspace nothing is split. */
+ * workspace holds; without a workspace nothing is split. Errors: F3C_EINVAL
+ * for a bad dtype, head_dim, q_prescaled, heads or batch, NULL pointers,
+ * leading dims below heads*head_dim or rows not 16-byte aligned, decreasing
+ * offsets, a sample with queries but no keys, a misaligned workspace, or (bf16,
+ * head_dim 64) one sample's key rows, rounded up to 64, spanning 2 GiB or more. */
 int f3c_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int32_t batch, const int32_t* q_off_host,
                      const int32_t* k_off_host, const void* q, int32_t ldq, const void* k, int32_t ldk,
                      const void* v, int32_t ldv, void* o, int32_t ldo, float* workspace, size_t workspace_bytes,

@@ -1016,6 +1016,13 @@ int f3c_op_attention(int32_t dtype, int32_t heads, int32_t head_dim, int32_t bat
     if (qs.off[b + 1] > qs.off[b] && ks.off[b + 1] == ks.off[b])
       return fail(F3C_EINVAL, "sample %d has queries but no keys", b);
   if (workspace && ((uintptr_t)workspace & 15)) return fail(F3C_EINVAL, "workspace must be 16-byte aligned");
+  if (dtype == F3C_BF16 && head_dim == 64) {
+    // the bf16 64-wide kernel addresses one sample's key and value rows with 32-bit offsets
+    int64_t nk_max = 0;
+    for (int b = 0; b < batch; ++b) nk_max = std::max<int64_t>(nk_max, ks.off[b + 1] - ks.off[b]);
+    const int64_t span = ((nk_max + 63) / 64) * 64 * (int64_t)std::max(ldk, ldv) * 2;
+    if (span >= (int64_t(1) << 31)) return fail(F3C_EINVAL, "one sample's key rows span 2 GiB or more");
+  }
   HIP_TRY(launch_attention(SITE_OP, dtype, heads, head_dim, qs, ks, q, ldq, k, ldk, v, ldv, o, ldo, workspace,
                            workspace ? workspace_bytes : 0, (hipStream_t)stream, q_prescaled == 1));
   return F3C_OK;

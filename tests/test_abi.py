@@ -155,6 +155,10 @@ def test_op_entry_validation_is_host_side(L):
     assert L.f3c_op_attention(1, 4, 64, 1, f3c._i32([0, 3]), f3c._i32([0, 3]), 16, 256, 16, 256, 16, 256, 16, 256,
                               4, 1024, 0, None) == f3c.F3C_EINVAL
     assert b"16-byte aligned" in L.f3c_last_error()
+    # bf16, 64-wide heads: one sample's key rows must span less than 2 GiB (32-bit DMA offsets)
+    assert L.f3c_op_attention(1, 1, 64, 1, f3c._i32([0, 1]), f3c._i32([0, 32768]), 16, 64, 16, 32768, 16, 64,
+                              16, 64, None, 0, 0, None) == f3c.F3C_EINVAL
+    assert b"2 GiB" in L.f3c_last_error()
     assert L.f3c_op_ln_mod(1, 4, 96, 1, None, None, 1, None) == f3c.F3C_EINVAL
     assert b"unsupported d" in L.f3c_last_error()
     m = f3c.Model(_cfg())                                   # no weights loaded
