@@ -18,10 +18,11 @@
 // bf16 conversion.
 //
 // Pipelining. bf16 with 64-wide heads (the transformer's case): K and V tiles
-// go from global memory straight into four LDS buffers with 16-byte DMA loads
-// issued three tiles ahead, and the score product of tile t+1 is issued before
-// the softmax and PV product of tile t, so the matrix cores have independent
-// work while the vector unit runs the softmax. Other types and head sizes
+// go from global memory straight into five LDS buffers (four with key groups)
+// with 16-byte DMA loads issued three tiles ahead (two with key groups), and
+// the score product of tile t+1 is issued before the softmax and PV product of
+// tile t, so the matrix cores have independent work while the vector unit runs
+// the softmax. Other types and head sizes
 // fetch the next tile into registers while the current one is consumed and
 // write it to the other of two LDS buffers. One barrier per tile either way.
 // Only the last, ragged tile is masked. The running max is updated lazily:
@@ -115,7 +116,8 @@ __global__ __launch_bounds__(64 * NW) void k_attn(AttnArgs p) {
   constexpr int ES = sizeof(T);
   constexpr int E = Mfma<T>::E;
   // bf16 with 64-wide heads: K and V tiles go global -> LDS directly (16-byte
-  // DMA loads, no registers) into four buffers, row-major with 128-byte rows
+  // DMA loads, no registers) into five buffers (four with key groups), row-major
+  // with 128-byte rows
   // whose 16-byte chunks are XOR-swizzled by row (conflict-free fragment
   // reads); V^T fragments come from the row-major V tile through the LDS
   // transpose read. Other types and head sizes stage through registers, with
